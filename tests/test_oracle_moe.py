@@ -1,0 +1,212 @@
+"""Pins for the oracle's MoE expert GEMM, SiLU gate, bf16 rounding and combine (CPU only)."""
+import math
+import struct
+from fractions import Fraction
+
+import numpy as np
+import pytest
+from scipy.special import expit
+
+import oracle
+import synth
+
+FMTS = [synth.FMT_Q8, synth.FMT_Q4]
+
+
+def bf16_value_struct(bits: int) -> float:
+    return struct.unpack(">f", struct.pack(">HH", int(bits), 0))[0]
+
+
+def small_moe(seed, T=9, E=5, topk=2, N=7, K=64, fmt=synth.FMT_Q4, skew=0.0):
+    rng = synth.rng_for(seed, T, E, topk, N, K, fmt)
+    x = synth.make_x(rng, T, K)
+    r = synth.make_routing(rng, T, E, topk, skew)
+    ws = [synth.make_qweight(rng, N, K, fmt) for _ in range(E)]
+    return x, r, ws
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_moe_exact_rational_tiny(fmt):
+    x, r, ws = small_moe(1, T=3, E=4, topk=2, N=3, K=32, fmt=fmt)
+    y, bound = oracle.moe(x, r.token_expert_idx, r.expert_offsets, [w.wq for w in ws],
+                          [w.scales for w in ws], 2, fmt)
+    for a in range(6):
+        t, e = a // 2, int(r.token_expert_idx[a])
+        for n in range(3):
+            terms = [Fraction(bf16_value_struct(x[t, k])) * Fraction(float(ws[e].scales[n, k // 32]))
+                     * int(ws[e].q[n, k]) for k in range(32)]
+            ex = sum(terms)
+            bx = sum(abs(v) for v in terms)
+            assert abs(Fraction(y[a, n]) - ex) <= 32 * 2.0 ** -52 * bx
+            assert abs(Fraction(bound[a, n]) - bx) <= 32 * 2.0 ** -52 * bx
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_moe_equals_token_major_dense_loop(fmt):
+    """Expert-major gather/scatter equals evaluating each (token, slot) with the dense oracle."""
+    x, r, ws = small_moe(2, T=17, E=6, topk=3, N=9, K=96, fmt=fmt)
+    y, bound = oracle.moe(x, r.token_expert_idx, r.expert_offsets, [w.wq for w in ws],
+                          [w.scales for w in ws], 3, fmt)
+    for a in range(17 * 3):
+        t, e = a // 3, int(r.token_expert_idx[a])
+        yd, bd = oracle.dense(x[t:t + 1], ws[e].wq, ws[e].scales, fmt)
+        np.testing.assert_allclose(y[a], yd[0], rtol=0, atol=96 * 2.0 ** -52 * bd.max())
+        np.testing.assert_allclose(bound[a], bd[0], rtol=1e-14)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_moe_ffn_weighted_per_expert_dense_loop(fmt):
+    """Grouped FFN output equals the router-weighted sum of per-expert dense evaluations."""
+    T, E, topk, hidden, inter = 11, 5, 2, 64, 32
+    rng = synth.rng_for(3, fmt)
+    x = synth.make_x(rng, T, hidden)
+    r = synth.make_routing(rng, T, E, topk)
+    wgu = [synth.make_qweight(rng, 2 * inter, hidden, fmt) for _ in range(E)]
+    wd = [synth.make_qweight(rng, hidden, inter, fmt) for _ in range(E)]
+    res = oracle.moe_ffn(x, r.token_expert_idx, r.expert_offsets, r.route_w,
+                         [w.wq for w in wgu], [w.scales for w in wgu],
+                         [w.wq for w in wd], [w.scales for w in wd], topk, inter, fmt)
+    for t in range(T):
+        acc = np.zeros(hidden)
+        for j in range(topk):
+            e = int(r.token_expert_idx[t * topk + j])
+            g, _ = oracle.dense(x[t:t + 1], wgu[e].wq, wgu[e].scales, fmt)
+            hv = [float(silu_scalar(g[0, i]) * g[0, inter + i]) for i in range(inter)]
+            hb = np.array([round_bf16_scalar(v) for v in hv])
+            y2, _ = oracle.dense(np.array([[bits_of(v) for v in hb]], dtype=np.uint16),
+                                 wd[e].wq, wd[e].scales, fmt)
+            acc += float(np.float32(r.route_w[t * topk + j])) * y2[0]
+        np.testing.assert_allclose(res["out"][t], acc, rtol=0, atol=1e-12 * res["bound_out"][t].max() + 1e-300)
+    tok = [0, 5, 10]
+    o2, b2 = oracle.moe_ffn_tokens(x, r.token_expert_idx, r.route_w, [w.wq for w in wgu], [w.scales for w in wgu],
+                                   [w.wq for w in wd], [w.scales for w in wd], topk, inter, fmt, tok)
+    np.testing.assert_allclose(o2, res["out"][tok], rtol=0, atol=1e-12 * res["bound_out"].max())
+    np.testing.assert_allclose(b2, res["bound_out"][tok], rtol=1e-12)
+
+
+def silu_scalar(z: float) -> float:
+    """Independent scalar SiLU via math.exp (stable branch per sign)."""
+    if z >= 0:
+        return z / (1.0 + math.exp(-z))
+    ez = math.exp(z)
+    return z * ez / (1.0 + ez)
+
+
+def round_bf16_scalar(v: float) -> float:
+    """Independent scalar RNE to 8 significant bits using exact rationals (normal range)."""
+    if v == 0:
+        return v
+    m, e = math.frexp(abs(v))                 # |v| = m * 2**e
+    scaled = Fraction(abs(v)) * Fraction(2) ** (8 - e)
+    fl = math.floor(scaled)
+    rem = scaled - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    return math.copysign(float(Fraction(fl) * Fraction(2) ** (e - 8)), v)
+
+
+def bits_of(v: float) -> int:
+    return struct.unpack(">I", struct.pack(">f", v))[0] >> 16
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_token_permutation_invariance(fmt):
+    x, r, ws = small_moe(4, T=13, E=5, topk=2, N=6, K=64, fmt=fmt)
+    wq, ss = [w.wq for w in ws], [w.scales for w in ws]
+    y, b = oracle.moe(x, r.token_expert_idx, r.expert_offsets, wq, ss, 2, fmt)
+    perm = synth.rng_for(5).permutation(13)
+    idx_p = r.token_expert_idx.reshape(13, 2)[perm].reshape(-1)
+    yp, _ = oracle.moe(x[perm], idx_p, synth.offsets_from_idx(idx_p, 5), wq, ss, 2, fmt)
+    rows = (perm[:, None] * 2 + np.arange(2)[None, :]).reshape(-1)
+    np.testing.assert_allclose(yp, y[rows], rtol=0, atol=64 * 2.0 ** -52 * b.max())
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_single_expert_topk1_equals_dense(fmt):
+    rng = synth.rng_for(6, fmt)
+    T, N, K = 10, 8, 64
+    x = synth.make_x(rng, T, K)
+    w = synth.make_qweight(rng, N, K, fmt)
+    r = synth.routing_from_idx(np.zeros(T, np.int32), 1, 1)
+    y, b = oracle.moe(x, r.token_expert_idx, r.expert_offsets, [w.wq], [w.scales], 1, fmt)
+    yd, bd = oracle.dense(x, w.wq, w.scales, fmt)
+    np.testing.assert_allclose(y, yd, rtol=0, atol=64 * 2.0 ** -52 * bd.max())
+    # every token on expert 0 of several experts, the others unused
+    ws = [w] + [synth.make_qweight(rng, N, K, fmt) for _ in range(3)]
+    r4 = synth.routing_from_idx(np.zeros(T, np.int32), 4, 1)
+    y4, _ = oracle.moe(x, r4.token_expert_idx, r4.expert_offsets, [v.wq for v in ws], [v.scales for v in ws], 1, fmt)
+    np.testing.assert_allclose(y4, yd, rtol=0, atol=64 * 2.0 ** -52 * bd.max())
+
+
+def test_empty_experts_are_never_touched():
+    """Experts with no routed tokens get NaN scales; the output stays finite."""
+    x, r, ws = small_moe(7, T=8, E=6, topk=1, N=5, K=32)
+    idx = np.array([0, 2, 2, 0, 5, 2, 0, 5], np.int32)
+    r = synth.routing_from_idx(idx, 6, 1)
+    ss = [w.scales.copy() for w in ws]
+    for e in (1, 3, 4):
+        ss[e][:] = np.float16(np.nan)
+    y, _ = oracle.moe(x, r.token_expert_idx, r.expert_offsets, [w.wq for w in ws], ss, 1, synth.FMT_Q4)
+    assert np.isfinite(y).all()
+
+
+def test_inconsistent_offsets_rejected():
+    x, r, ws = small_moe(8)
+    bad = r.expert_offsets.copy()
+    bad[1] += 1
+    with pytest.raises(ValueError):
+        oracle.moe(x, r.token_expert_idx, bad, [w.wq for w in ws], [w.scales for w in ws], 2, synth.FMT_Q4)
+
+
+def test_silu_closed_forms():
+    assert oracle.silu(0.0) == 0.0
+    z = np.linspace(-30, 30, 1001)
+    np.testing.assert_allclose(oracle.silu(z) - oracle.silu(-z), z, rtol=0, atol=1e-13)
+    big = np.array([40.0, 100.0, 1e3])
+    assert np.array_equal(oracle.silu(big), big)
+    assert np.all(oracle.silu(-big) <= 0) and np.all(oracle.silu(-big) > -1e-15)
+    np.testing.assert_allclose(oracle.silu(z), z * expit(z), rtol=1e-14, atol=1e-300)
+    assert abs(oracle.silu(1.0) - 1 / (1 + math.exp(-1))) < 1e-16
+
+
+def test_bf16_rounding_closed_forms():
+    vals = np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, 1 + 2.0 ** -8 + 2.0 ** -30, -(1 + 2.0 ** -8),
+                     2.0 ** -134, 3 * 2.0 ** -134, 1e39, -1e39, 0.0, 2.0 ** -126 * (1 + 2.0 ** -8)])
+    out, bits = oracle.round_to_bf16(vals)
+    assert out[0] == 1.0                      # tie -> even
+    assert out[1] == 1 + 2.0 ** -6            # tie -> even (up)
+    assert out[2] == 1 + 2.0 ** -7            # above the tie
+    assert out[3] == -1.0
+    assert out[4] == 0.0                      # subnormal tie -> even (zero)
+    assert out[5] == 2.0 ** -132              # subnormal tie -> even (up)
+    assert out[6] == math.inf and out[7] == -math.inf
+    assert out[8] == 0.0
+    assert out[9] == 2.0 ** -126              # smallest normal, tie -> even
+    assert bits[0] == 0x3F80 and bits[3] == 0xBF80 and bits[6] == 0x7F80
+
+
+def test_bf16_rounding_matches_torch_and_scalar_rule():
+    torch = pytest.importorskip("torch")
+    v = synth.rng_for(9).standard_normal(20000) * np.exp(synth.rng_for(10).uniform(-20, 20, 20000))
+    v32 = v.astype(np.float32).astype(np.float64)      # float32-representable: torch rounds once
+    out, bits = oracle.round_to_bf16(v32)
+    ref = torch.from_numpy(v32.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(out, ref)
+    for val in v[:300]:
+        assert oracle.round_to_bf16(np.array([val]))[0][0] == round_bf16_scalar(float(val))
+
+
+def test_combine_closed_forms():
+    T, topk, N = 4, 3, 5
+    y2 = synth.rng_for(11).standard_normal((T * topk, N))
+    w = np.zeros(T * topk, np.float32)
+    w[np.arange(T) * topk + 1] = 1.0
+    out, _ = oracle.combine(y2, w, topk)
+    assert np.array_equal(out, y2[np.arange(T) * topk + 1])
+    same = np.repeat(y2[::topk], topk, axis=0)
+    w2 = np.array([0.25, 0.25, 0.5] * T, np.float32)
+    out2, _ = oracle.combine(same, w2, topk)
+    assert np.array_equal(out2, y2[::topk])
+    b = np.abs(y2)
+    _, bnd = oracle.combine(y2, -w2, topk, b)
+    np.testing.assert_allclose(bnd, (b.reshape(T, topk, N) * np.array([0.25, 0.25, 0.5])[None, :, None]).sum(1))
