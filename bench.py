@@ -1,0 +1,275 @@
+#!/usr/bin/env python3
+"""Throughput of the block-quantised prefill GEMM path on one MI355X.
+
+One step is one pass of the whole path over the 2048+-token prefill workloads:
+
+* dense Q8 gate/up projection, M=2048 tokens, K=2048, N=8192;
+* dense Q8 down projection, M=2048, K=8192, N=2048;
+* MoE Q4 FFN, T=2048 tokens, E=128 experts, top-8 (uniform router logits):
+  bucket token slots by expert, gate/up grouped GEMM (K=2048, N=1536),
+  SiLU-gated activation, down grouped GEMM (K=768, N=2048), router-weighted combine;
+* the same MoE FFN at T=8192 with Zipf-skewed routing (groups of 0 to ~8000 rows).
+
+``value`` = algorithmic GEMM FLOP per step (2*M*N*K per dense GEMM, 2*(T*topk)*N*K
+per grouped GEMM; padding and inactive experts are not counted) / wall time per
+step, with every input resident in HBM. The JSON line also carries the roofline
+of the dominant kernel (per-launch HIP event timing inside the timed region) and
+the CPU oracle's throughput on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+METRIC = "prefill quantized GEMM TFLOP/s (dense + MoE) and % of MI355X bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2516.6      # 256 CUs x 4096 dense bf16 FLOP/clk x 2.4 GHz
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-seconds", type=float, default=15.0)
+    ap.add_argument("--only", default="", help="comma list of parts to run: dense_gate_up,dense_down,moe_t2048,moe_t8192")
+    return ap.parse_args()
+
+
+class Part:
+    def __init__(self, name, flops):
+        self.name = name
+        self.flops = flops
+
+
+def build_parts(torch, q, synth, only):
+    """Device-resident inputs and output buffers for every part of the step."""
+    dev = torch.device("cuda:0")
+
+    def x_dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    parts = []
+    want = set(only.split(",")) if only else None
+    dense_cases = synth.config(2)
+    for tag, case in zip(("dense_gate_up", "dense_down"), dense_cases):
+        if want and tag not in want:
+            continue
+        p = Part(tag, case.flops)
+        p.kind = "dense"
+        p.x = x_dev(case.x)
+        p.wq = torch.from_numpy(case.w.wq).to(dev)
+        p.sc = torch.from_numpy(case.w.scales).to(dev)
+        p.y = torch.empty((case.M, case.N), dtype=torch.float32, device=dev)
+        p.fmt = case.fmt
+        p.case = case
+        p.gemm_flops = {"dense": case.flops}
+        parts.append(p)
+    for tag, cfg in (("moe_t2048", 3), ("moe_t8192", 4)):
+        if want and tag not in want:
+            continue
+        (case,) = synth.config(cfg)
+        r = case.routing
+        A = case.T * case.topk
+        p = Part(tag, case.flops_gate_up + case.flops_down)
+        p.kind = "moe"
+        p.case = case
+        p.fmt = case.fmt
+        p.x = x_dev(case.x)
+        p.idx = torch.from_numpy(r.token_expert_idx).to(dev)
+        p.off = torch.from_numpy(r.expert_offsets).to(dev)
+        p.rw = torch.from_numpy(r.route_w).to(dev)
+        p.wgu = torch.from_numpy(np.stack([w.wq for w in case.w_gate_up])).to(dev)
+        p.sgu = torch.from_numpy(np.stack([w.scales for w in case.w_gate_up])).to(dev)
+        p.wd = torch.from_numpy(np.stack([w.wq for w in case.w_down])).to(dev)
+        p.sd = torch.from_numpy(np.stack([w.scales for w in case.w_down])).to(dev)
+        p.wgu_l, p.sgu_l = list(p.wgu.unbind(0)), list(p.sgu.unbind(0))
+        p.wd_l, p.sd_l = list(p.wd.unbind(0)), list(p.sd.unbind(0))
+        p.perm = torch.empty((A,), dtype=torch.int32, device=dev)
+        p.y1 = torch.empty((A, 2 * case.inter), dtype=torch.float32, device=dev)
+        p.h = torch.empty((A, case.inter), dtype=torch.bfloat16, device=dev)
+        p.y2 = torch.empty((A, case.hidden), dtype=torch.float32, device=dev)
+        p.out = torch.empty((case.T, case.hidden), dtype=torch.float32, device=dev)
+        p.gemm_flops = {"gate_up": case.flops_gate_up, "down": case.flops_down}
+        parts.append(p)
+        del case.w_gate_up, case.w_down
+    return parts
+
+
+def run_part(q, p, timer=None):
+    """Enqueue one pass of a part; `timer(name)` returns a context that brackets a GEMM launch with events."""
+    if p.kind == "dense":
+        with timer(p.name + ":dense"):
+            q.dense(p.x, p.wq, p.sc, p.fmt, out=p.y)
+        return
+    c = p.case
+    q.moe_bucket(p.idx, p.off, out=p.perm)
+    with timer(p.name + ":gate_up"):
+        q.moe_grouped(p.x, p.perm, p.off, p.wgu_l, p.sgu_l, c.topk, c.fmt, out=p.y1)
+    q.swiglu(p.y1, out=p.h)
+    with timer(p.name + ":down"):
+        q.moe_grouped(p.h, p.perm, p.off, p.wd_l, p.sd_l, 1, c.fmt, out=p.y2)
+    q.moe_combine(p.y2, p.rw, c.topk, out=p.out)
+
+
+class EventTimer:
+    """Per-launch HIP events on the launching stream, accumulated over the timed region."""
+
+    def __init__(self, torch, enabled):
+        self.torch = torch
+        self.enabled = enabled
+        self.pending = []
+
+    def __call__(self, name):
+        timer = self
+
+        class _Ctx:
+            def __enter__(self_inner):
+                if timer.enabled:
+                    self_inner.s = timer.torch.cuda.Event(enable_timing=True)
+                    self_inner.e = timer.torch.cuda.Event(enable_timing=True)
+                    self_inner.s.record(timer.torch.cuda.current_stream())
+
+            def __exit__(self_inner, *exc):
+                if timer.enabled:
+                    self_inner.e.record(timer.torch.cuda.current_stream())
+                    timer.pending.append((name, self_inner.s, self_inner.e))
+                return False
+
+        return _Ctx()
+
+    def summary(self):
+        out = {}
+        for name, s, e in self.pending:
+            out.setdefault(name, []).append(s.elapsed_time(e))
+        return {k: float(np.mean(v)) for k, v in out.items()}
+
+
+def cpu_baseline(synth, seconds):
+    """The oracle as it stands, on a bounded sample of the same workload, on this host's cores."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl missing
+        threads = len(os.sched_getaffinity(0))
+    (gate_up, down) = synth.config(2)
+    flops = 0.0
+    spent = 0.0
+    rows = 32
+    done = []
+    # dense gate/up rows in growing slices until the time budget is half used
+    t0 = time.perf_counter()
+    oracle.dense(gate_up.x[:rows], gate_up.w.wq, gate_up.w.scales, gate_up.fmt)
+    dt = time.perf_counter() - t0
+    flops += 2.0 * rows * gate_up.N * gate_up.K
+    spent += dt
+    done.append(f"dense Q8 gate_up rows 0..{rows}")
+    # MoE: the first tokens of the T=2048 workload through the gate/up expert GEMM
+    (moe,) = synth.config(3)
+    r = moe.routing
+    T_s = 16
+    while spent < seconds:
+        A = T_s * moe.topk
+        idx = r.token_expert_idx[:A]
+        off = synth.offsets_from_idx(idx, moe.E)
+        t0 = time.perf_counter()
+        oracle.moe(moe.x[:T_s], idx, off, [w.wq for w in moe.w_gate_up], [w.scales for w in moe.w_gate_up],
+                   moe.topk, moe.fmt)
+        dt = time.perf_counter() - t0
+        flops += 2.0 * A * 2 * moe.inter * moe.hidden
+        spent += dt
+        done.append(f"MoE Q4 gate_up, tokens 0..{T_s}")
+        T_s *= 2
+        if spent + 2.2 * dt > 2 * seconds:
+            break
+    return {"value": flops / spent / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": "; ".join(done) + f" ({spent:.1f} s of fp64 CPU work; FLOP counted as 2*M*N*K of the sampled rows)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        log("only --gpus 1 is supported: the path is a single-GPU kernel library")
+        return 2
+    import torch
+    import paper_2607_19438_amd as q
+    import synth
+    if not torch.cuda.is_available():
+        log("no GPU visible")
+        return 1
+    q.lib()
+    log("generating inputs")
+    t0 = time.perf_counter()
+    parts = build_parts(torch, q, synth, args.only)
+    torch.cuda.synchronize()
+    log(f"inputs resident in HBM ({time.perf_counter() - t0:.1f} s)")
+    plain = EventTimer(torch, False)
+    for _ in range(args.warmup):
+        for p in parts:
+            run_part(q, p, plain)
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    # timed region: whole-job wall time, with per-launch events on the launching stream
+    timer = EventTimer(torch, True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        for p in parts:
+            run_part(q, p, timer)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    log(f"timed {args.steps} steps in {wall:.3f} s")
+    ms_per_step = wall / args.steps * 1e3
+    flops_step = sum(p.flops for p in parts)
+    value = flops_step / (wall / args.steps) / 1e12
+
+    per = timer.summary()
+    flops_of = {}
+    for p in parts:
+        for k, f in p.gemm_flops.items():
+            flops_of[f"{p.name}:{k}"] = f
+    breakdown = {k: {"ms": per[k], "tflops": flops_of[k] / (per[k] * 1e-3) / 1e12,
+                     "frac_mfma": flops_of[k] / (per[k] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS} for k in per}
+    dom = max(per, key=lambda k: per[k])
+    achieved = flops_of[dom] / (per[dom] * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None, "kernel": dom}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(synth, args.cpu_sample_seconds)
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "prefill_2048: dense Q8 gate_up 2048x8192x2048 + dense Q8 down 2048x2048x8192 + "
+                               "MoE Q4 FFN T=2048 E=128 top8 + MoE Q4 FFN T=8192 E=128 top8 Zipf-skewed"
+                               if not args.only else args.only,
+                   "frac_of_mfma_peak": value / PEAK_BF16_TFLOPS, "flop_per_step": flops_step},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "breakdown": breakdown,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

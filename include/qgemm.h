@@ -1,0 +1,149 @@
+/*
+ * qgemm.h - C ABI of the MI355X (gfx950) block-quantised prefill GEMM library.
+ *
+ * The library computes the prompt-processing (prefill) matrix multiplies the
+ * paper routes onto matrix units (Section 3.1): dense projection GEMMs over
+ * 4-bit / 8-bit block-quantised weights, and the MoE expert GEMM that
+ * evaluates each active expert's projection over the tokens routed to it,
+ * plus the SiLU-gated activation between the MoE projections (Section 3.1,
+ * fused gate/up item) and the router-weighted combine of the experts' outputs.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers are DEVICE pointers (memory the HIP runtime of this process
+ *   allocated on the current device) unless the comment says HOST.
+ * - Arrays are dense and row-major; no strides. Every device pointer must be
+ *   16-byte aligned (QGEMM_EALIGN otherwise).
+ * - Work is enqueued on `stream` (0 = the null stream) and the call returns
+ *   without synchronising; device faults surface at the caller's next sync.
+ *   The caller keeps every buffer alive until the stream has passed the call.
+ * - Outputs are written, never accumulated into, and must not alias inputs.
+ * - Return value: QGEMM_OK (0) or a negative QGEMM_E* code. On an error return
+ *   nothing has been enqueued and no output is written;
+ *   qgemm_last_error() gives a message. No entry point throws.
+ * - A zero-sized problem (M, T or rows == 0) returns QGEMM_OK and launches
+ *   nothing.
+ *
+ * Storage formats (the paper names 4-bit and 8-bit block quantisation without a
+ * byte layout; this is the layout the library reads):
+ * - activations x: bf16 [rows][K].
+ * - QGEMM_Q8 weights: int8 [N][K]; element (n, k) means q * s.
+ * - QGEMM_Q4 weights: uint8 [N][K/2]; byte j of a row holds element 2j in
+ *   bits 0-3 and element 2j+1 in bits 4-7; a nibble u means (u - 8) * s.
+ * - scales: fp16 [N][K/32]; s = scales[n][k / 32] (one scale per 32
+ *   consecutive K elements of a row).
+ * - K must be a multiple of 32.
+ * - results: fp32, y[m][n] = sum_k x[m][k] * s[n][k/32] * q[n][k]; the
+ *   library rounds each dequantised weight to bf16 and accumulates in fp32.
+ */
+#ifndef QGEMM_H
+#define QGEMM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#ifndef __HIP_INCLUDE_HIP_HIP_RUNTIME_API_H__
+typedef struct ihipStream_t* hipStream_t;
+#endif
+
+enum qgemm_fmt { QGEMM_Q8 = 0, QGEMM_Q4 = 1 };
+
+enum qgemm_status {
+  QGEMM_OK = 0,
+  QGEMM_EINVAL = -1,       /* bad size, format, null pointer or routing table */
+  QGEMM_EALIGN = -2,       /* a device pointer is not 16-byte aligned */
+  QGEMM_EUNSUPPORTED = -3, /* a size beyond what the library handles */
+  QGEMM_EHIP = -4          /* the HIP runtime reported an error */
+};
+
+/*
+ * Dense block-quantised GEMM (Section 3.1, dense GEMM item):
+ *   y[M][N] = x[M][K] . dequant(wq, scales)^T
+ * x: bf16 [M][K]; wq: int8 [N][K] (Q8) or uint8 [N][K/2] (Q4);
+ * scales: fp16 [N][K/32]; y: fp32 [M][N].
+ * Sizes: M >= 0, 1 <= N, 32 <= K, K % 32 == 0, every element count < 2^31.
+ */
+int qgemm_dense(const void* x, const void* wq, const void* scales, float* y,
+                int M, int N, int K, int fmt, hipStream_t stream);
+
+/*
+ * MoE expert GEMM (Section 3.1, MoE expert GEMM item): every token slot
+ * ("assignment") a = t*topk + j is multiplied by the weights of its expert:
+ *   y[a][:] = dequant(wq[e], scales[e]) . x[a / topk][:],  e = token_expert_idx[a]
+ * Only experts with at least one assignment read their weights.
+ * x: bf16 [T][K].
+ * token_expert_idx: int32 [T*topk], values in [0, E).
+ * expert_offsets: int32 [E+1], exclusive prefix sum of the per-expert
+ *   assignment counts (offsets[0] == 0, offsets[E] == T*topk).
+ * wq, scales: HOST arrays of E device pointers, each laid out as for
+ *   qgemm_dense with the same N and K.
+ * y: fp32 [T*topk][N], in assignment (token-slot) order.
+ * Sizes: 1 <= E <= 65536, 1 <= topk <= E, T*topk < 2^31.
+ * The call buckets the assignments by expert into a library-owned workspace
+ * (grown on first use, then reused; freed by qgemm_release) and runs the
+ * grouped GEMM. Routing tables that disagree with each other are a caller
+ * error: every access stays in bounds, and the rows of y that depend on the
+ * inconsistent expert are written as NaN. With the environment variable
+ * QGEMM_VALIDATE=1 the call synchronises `stream` and returns QGEMM_EINVAL
+ * in that case.
+ * Calls that share the workspace are ordered only by their streams: do not
+ * run two qgemm_moe calls concurrently on different streams.
+ */
+int qgemm_moe(const void* x, const int32_t* token_expert_idx,
+              const int32_t* expert_offsets, const void* const* wq,
+              const void* const* scales, float* y, int T, int E, int topk,
+              int N, int K, int fmt, hipStream_t stream);
+
+/*
+ * The two halves of qgemm_moe, for callers that keep their own bucketing
+ * buffer (the MoE expert GEMM of Section 3.1 needs each expert's routed
+ * token list).
+ * qgemm_moe_bucket: perm: int32 [n_assign], caller-owned. Writes the
+ *   assignments grouped by expert: perm[expert_offsets[e] + r] is the r-th
+ *   assignment (in increasing order) routed to expert e. Stable and
+ *   deterministic. Entries for an expert whose count disagrees with
+ *   expert_offsets are written as -1.
+ * qgemm_moe_grouped: same arguments as qgemm_moe with perm in place of
+ *   token_expert_idx; perm entries outside [0, T*topk) are skipped.
+ */
+int qgemm_moe_bucket(const int32_t* token_expert_idx, const int32_t* expert_offsets,
+                     int32_t* perm, int n_assign, int E, hipStream_t stream);
+int qgemm_moe_grouped(const void* x, const int32_t* perm, const int32_t* expert_offsets,
+                      const void* const* wq, const void* const* scales, float* y,
+                      int T, int E, int topk, int N, int K, int fmt, hipStream_t stream);
+
+/*
+ * SiLU-gated activation between the MoE projections (Section 3.1, fused
+ * gate/up item): for r < rows, i < inter,
+ *   h[r][i] = bf16_rne(silu(y1[r][i]) * y1[r][inter + i]),  silu(z) = z / (1 + e^-z)
+ * y1: fp32 [rows][2*inter]; h: bf16 [rows][inter]. inter % 8 == 0.
+ */
+int qgemm_swiglu(const float* y1, void* h, int rows, int inter, hipStream_t stream);
+
+/*
+ * Router-weighted combine of the selected experts' outputs:
+ *   out[t][n] = sum_{j < topk} route_w[t*topk + j] * y2[t*topk + j][n]
+ * summed in increasing j in fp32. y2: fp32 [T*topk][N]; route_w: fp32
+ * [T*topk]; out: fp32 [T][N]. N % 4 == 0.
+ */
+int qgemm_moe_combine(const float* y2, const float* route_w, float* out,
+                      int T, int topk, int N, hipStream_t stream);
+
+/* Message of the last non-OK return on the calling thread ("" if none). */
+const char* qgemm_last_error(void);
+
+/* Frees the library-owned MoE workspace (the next qgemm_moe grows it again).
+ * The caller must have synchronised every stream that used it. */
+int qgemm_release(void);
+
+/* Library ABI version, (major << 16) | minor. */
+int qgemm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QGEMM_H */

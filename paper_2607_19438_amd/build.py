@@ -1,0 +1,52 @@
+"""Build the gfx950 shared library ``libqgemm.so`` in-tree with hipcc.
+
+Usage: ``python -m paper_2607_19438_amd.build [--verbose]``.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(HERE, "csrc")
+LIB = os.path.join(HERE, "libqgemm.so")
+SOURCES = [os.path.join(CSRC, "qgemm_api.hip")]
+DEPS = SOURCES + [os.path.join(CSRC, f) for f in ("qgemm_kernels.hpp", "qgemm_aux.hpp")] + [
+    os.path.join(os.path.dirname(HERE), "include", "qgemm.h")]
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+
+FLAGS = [
+    f"--offload-arch={ARCH}",
+    "-O3",
+    "-std=c++17",
+    "-fPIC",
+    "-shared",
+    # no packed-fp32 VALU instructions in any device code
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall",
+    "-Wno-unused-command-line-argument",
+]
+
+
+def build(verbose: bool = False, extra=None) -> str:
+    cmd = [HIPCC, *FLAGS, *(extra or []), *SOURCES, "-o", LIB + ".tmp"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    out = "\n".join(l for l in (res.stdout + res.stderr).splitlines()
+                    if "not a recognized feature" not in l)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{out}")
+    if verbose and out.strip():
+        print(out)
+    os.replace(LIB + ".tmp", LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    v = "--verbose" in sys.argv
+    extra = ["-Rpass-analysis=kernel-resource-usage"] if "--resources" in sys.argv else None
+    print(build(verbose=v or bool(extra), extra=extra))

@@ -1,0 +1,384 @@
+// C ABI of the block-quantised prefill GEMM library (declarations and the
+// contract of every entry point are in include/qgemm.h).
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/qgemm.h"
+#include "qgemm_kernels.hpp"
+#include "qgemm_aux.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int ok() {
+  g_last_error.clear();
+  return QGEMM_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(QGEMM_EHIP, "%s: kernel launch failed: %s", what, hipGetErrorString(e));
+  return QGEMM_OK;
+}
+
+int check_common(int N, int K, int fmt) {
+  if (fmt != QGEMM_Q8 && fmt != QGEMM_Q4) return fail(QGEMM_EINVAL, "unknown weight format %d", fmt);
+  if (N < 1) return fail(QGEMM_EINVAL, "N must be >= 1 (got %d)", N);
+  if (K < 32 || K % 32 != 0) return fail(QGEMM_EINVAL, "K must be a positive multiple of 32 (got %d)", K);
+  return QGEMM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// kernel selection
+// ---------------------------------------------------------------------------
+
+template <int FMT, int BM, int BN, int WM, int WN>
+int launch_dense(const qg::TileArgs& a, const void* wq, const void* sc, hipStream_t s) {
+  const long tiles = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  if (tiles > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "too many tiles");
+  hipLaunchKernelGGL((qg::dense_kernel<FMT, BM, BN, WM, WN>), dim3((unsigned)tiles), dim3(WM * WN * 64), 0, s, a,
+                     static_cast<const uint8_t*>(wq), static_cast<const uint16_t*>(sc));
+  return check_launch("qgemm_dense");
+}
+
+template <int FMT>
+int dense_dispatch(const qg::TileArgs& a, const void* wq, const void* sc, hipStream_t s) {
+  const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
+  if (a.M >= 256 && a.N >= 256 && big >= 200) return launch_dense<FMT, 256, 256, 2, 2>(a, wq, sc, s);
+  return launch_dense<FMT, 128, 128, 2, 2>(a, wq, sc, s);
+}
+
+constexpr int kMoeBM = 128;
+constexpr int kMoeBN = 128;
+
+template <int FMT>
+int launch_moe(qg::TileArgs a, const void* const* wq, const void* const* sc, int E, hipStream_t s) {
+  const int nt = (a.N + kMoeBN - 1) / kMoeBN;
+  for (int e0 = 0; e0 < E; e0 += qg::kMaxExpertsPerLaunch) {
+    const int ne = (E - e0) < qg::kMaxExpertsPerLaunch ? (E - e0) : qg::kMaxExpertsPerLaunch;
+    qg::ExpertPtrs ep;
+    for (int i = 0; i < qg::kMaxExpertsPerLaunch; ++i) {
+      ep.wq[i] = i < ne ? static_cast<const uint8_t*>(wq[e0 + i]) : nullptr;
+      ep.sc[i] = i < ne ? static_cast<const uint16_t*>(sc[e0 + i]) : nullptr;
+    }
+    a.e_begin = e0;
+    a.n_experts = ne;
+    // upper bound of sum_e ceil(c_e / BM) over the launch's experts
+    const long mt_bound = (long)(a.M + kMoeBM - 1) / kMoeBM + ne;
+    const long grid = mt_bound * nt;
+    if (grid > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "too many tiles");
+    hipLaunchKernelGGL((qg::moe_kernel<FMT, kMoeBM, kMoeBN, 2, 2>), dim3((unsigned)grid), dim3(256), 0, s, a, ep);
+    const int rc = check_launch("qgemm_moe");
+    if (rc != QGEMM_OK) return rc;
+  }
+  return QGEMM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// MoE workspace (per device): bucketing output, per-block counts, error flag
+// ---------------------------------------------------------------------------
+
+struct Workspace {
+  int32_t* perm = nullptr;
+  size_t perm_cap = 0;
+  int32_t* counts = nullptr;
+  size_t counts_cap = 0;
+  int32_t* flag = nullptr;
+  int seq = 0;
+};
+
+std::mutex g_ws_mutex;
+std::vector<Workspace> g_ws;
+
+int grow(int32_t** p, size_t* cap, size_t need) {
+  if (*cap >= need) return QGEMM_OK;
+  if (*p != nullptr) {
+    (void)hipFree(*p);   // hipFree waits for outstanding work that may still read the buffer
+    *p = nullptr;
+    *cap = 0;
+  }
+  size_t want = need < 4096 ? 4096 : need;
+  if (hipMalloc(reinterpret_cast<void**>(p), want * sizeof(int32_t)) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(QGEMM_EHIP, "hipMalloc of %zu bytes for the MoE workspace failed", want * sizeof(int32_t));
+  }
+  *cap = want;
+  return QGEMM_OK;
+}
+
+int bucket_geometry(int n, int* chunk, int* nblk) {
+  int c = 4096;
+  long nb = ((long)n + c - 1) / c;
+  if (nb > 1024) {
+    c = (int)((((long)n + 1023) / 1024 + 255) / 256 * 256);
+    nb = ((long)n + c - 1) / c;
+  }
+  *chunk = c;
+  *nblk = (int)nb;
+  return QGEMM_OK;
+}
+
+constexpr int kMaxE = 4096;
+
+int enqueue_bucket(const int32_t* idx, const int32_t* offsets, int32_t* perm, int n, int E, int32_t* counts,
+                   int32_t* flag, int seq, float* ypoison, int N, hipStream_t s) {
+  int chunk, nblk;
+  bucket_geometry(n, &chunk, &nblk);
+  const size_t lds = (size_t)E * sizeof(int32_t);
+  hipLaunchKernelGGL(qg::bucket_count_kernel, dim3(nblk), dim3(qg::kBucketThreads), lds, s, idx, n, E, chunk, counts);
+  int rc = check_launch("moe bucket count");
+  if (rc != QGEMM_OK) return rc;
+  hipLaunchKernelGGL(qg::bucket_scatter_kernel, dim3(nblk), dim3(qg::kBucketThreads), lds, s, idx, offsets, n, E,
+                     chunk, counts, nblk, perm, flag, seq, ypoison, N);
+  return check_launch("moe bucket scatter");
+}
+
+Workspace* workspace_for_current_device(int* dev_out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  if ((int)g_ws.size() <= dev) g_ws.resize(dev + 1);
+  *dev_out = dev;
+  return &g_ws[dev];
+}
+
+int moe_args_check(const void* x, const void* idx_or_perm, const int32_t* offsets, const void* const* wq,
+                   const void* const* scales, const float* y, int T, int E, int topk, int N, int K, int fmt) {
+  int rc = check_common(N, K, fmt);
+  if (rc != QGEMM_OK) return rc;
+  if (T < 0) return fail(QGEMM_EINVAL, "T must be >= 0 (got %d)", T);
+  if (E < 1) return fail(QGEMM_EINVAL, "E must be >= 1 (got %d)", E);
+  if (E > kMaxE) return fail(QGEMM_EUNSUPPORTED, "E = %d exceeds the supported %d experts", E, kMaxE);
+  if (topk < 1 || topk > E) return fail(QGEMM_EINVAL, "topk must lie in [1, E] (got %d)", topk);
+  if ((long)T * topk > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "T*topk too large");
+  if ((long)T * topk * N > 0x7fffffffffffL || (long)T * K > 0x7fffffffL)
+    return fail(QGEMM_EUNSUPPORTED, "problem too large");
+  if (T == 0) return QGEMM_OK;
+  if (!x || !idx_or_perm || !offsets || !wq || !scales || !y) return fail(QGEMM_EINVAL, "null pointer argument");
+  if (!aligned16(x) || !aligned16(y) || !aligned16(idx_or_perm) || !aligned16(offsets))
+    return fail(QGEMM_EALIGN, "x, y and routing tables must be 16-byte aligned");
+  for (int e = 0; e < E; ++e) {
+    if (!wq[e] || !scales[e]) return fail(QGEMM_EINVAL, "null weight or scale pointer for expert %d", e);
+    if (!aligned16(wq[e])) return fail(QGEMM_EALIGN, "weights of expert %d are not 16-byte aligned", e);
+    if ((reinterpret_cast<uintptr_t>(scales[e]) & 1u) != 0)
+      return fail(QGEMM_EALIGN, "scales of expert %d are not 2-byte aligned", e);
+  }
+  return QGEMM_OK;
+}
+
+bool validate_env() {
+  const char* v = getenv("QGEMM_VALIDATE");
+  return v != nullptr && v[0] == '1';
+}
+
+}  // namespace
+
+extern "C" {
+
+int qgemm_version(void) { return (1 << 16) | 0; }
+
+const char* qgemm_last_error(void) { return g_last_error.c_str(); }
+
+int qgemm_dense(const void* x, const void* wq, const void* scales, float* y, int M, int N, int K, int fmt,
+                hipStream_t stream) {
+  int rc = check_common(N, K, fmt);
+  if (rc != QGEMM_OK) return rc;
+  if (M < 0) return fail(QGEMM_EINVAL, "M must be >= 0 (got %d)", M);
+  if ((long)M * K > 0x7fffffffL || (long)N * K > 0x7fffffffL || (long)M * N > 0x7fffffffL)
+    return fail(QGEMM_EUNSUPPORTED, "an operand has 2^31 or more elements");
+  if (M == 0) return ok();
+  if (!x || !wq || !scales || !y) return fail(QGEMM_EINVAL, "null pointer argument");
+  if (!aligned16(x) || !aligned16(wq) || !aligned16(y))
+    return fail(QGEMM_EALIGN, "x, wq and y must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(scales) & 1u) != 0) return fail(QGEMM_EALIGN, "scales must be 2-byte aligned");
+  (void)hipGetLastError();
+  qg::TileArgs a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.y = y;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  rc = (fmt == QGEMM_Q8) ? dense_dispatch<qg::kQ8>(a, wq, scales, stream)
+                         : dense_dispatch<qg::kQ4>(a, wq, scales, stream);
+  return rc == QGEMM_OK ? ok() : rc;
+}
+
+int qgemm_moe_bucket(const int32_t* token_expert_idx, const int32_t* expert_offsets, int32_t* perm, int n_assign,
+                     int E, hipStream_t stream) {
+  if (n_assign < 0) return fail(QGEMM_EINVAL, "n_assign must be >= 0");
+  if (E < 1) return fail(QGEMM_EINVAL, "E must be >= 1");
+  if (E > kMaxE) return fail(QGEMM_EUNSUPPORTED, "E = %d exceeds the supported %d experts", E, kMaxE);
+  if (n_assign == 0) return ok();
+  if (!token_expert_idx || !expert_offsets || !perm) return fail(QGEMM_EINVAL, "null pointer argument");
+  if (!aligned16(token_expert_idx) || !aligned16(expert_offsets) || !aligned16(perm))
+    return fail(QGEMM_EALIGN, "routing tables must be 16-byte aligned");
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  int dev;
+  Workspace* ws = workspace_for_current_device(&dev);
+  if (!ws) return fail(QGEMM_EHIP, "hipGetDevice failed");
+  int chunk, nblk;
+  bucket_geometry(n_assign, &chunk, &nblk);
+  int rc = grow(&ws->counts, &ws->counts_cap, (size_t)nblk * E);
+  if (rc != QGEMM_OK) return rc;
+  size_t one = 0;
+  if (ws->flag == nullptr) {
+    rc = grow(&ws->flag, &one, 1);
+    if (rc != QGEMM_OK) return rc;
+  }
+  (void)hipGetLastError();
+  rc = enqueue_bucket(token_expert_idx, expert_offsets, perm, n_assign, E, ws->counts, ws->flag, 0, nullptr, 0,
+                      stream);
+  return rc == QGEMM_OK ? ok() : rc;
+}
+
+int qgemm_moe_grouped(const void* x, const int32_t* perm, const int32_t* expert_offsets, const void* const* wq,
+                      const void* const* scales, float* y, int T, int E, int topk, int N, int K, int fmt,
+                      hipStream_t stream) {
+  int rc = moe_args_check(x, perm, expert_offsets, wq, scales, y, T, E, topk, N, K, fmt);
+  if (rc != QGEMM_OK || T == 0) return rc == QGEMM_OK ? ok() : rc;
+  (void)hipGetLastError();
+  qg::TileArgs a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.y = y;
+  a.M = T * topk;
+  a.N = N;
+  a.K = K;
+  a.perm = perm;
+  a.offsets = expert_offsets;
+  a.topk = topk;
+  a.T = T;
+  rc = (fmt == QGEMM_Q8) ? launch_moe<qg::kQ8>(a, wq, scales, E, stream)
+                         : launch_moe<qg::kQ4>(a, wq, scales, E, stream);
+  return rc == QGEMM_OK ? ok() : rc;
+}
+
+int qgemm_moe(const void* x, const int32_t* token_expert_idx, const int32_t* expert_offsets, const void* const* wq,
+              const void* const* scales, float* y, int T, int E, int topk, int N, int K, int fmt,
+              hipStream_t stream) {
+  int rc = moe_args_check(x, token_expert_idx, expert_offsets, wq, scales, y, T, E, topk, N, K, fmt);
+  if (rc != QGEMM_OK || T == 0) return rc == QGEMM_OK ? ok() : rc;
+  const int n = T * topk;
+  int seq;
+  int32_t* perm;
+  int32_t* flag;
+  {
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    int dev;
+    Workspace* ws = workspace_for_current_device(&dev);
+    if (!ws) return fail(QGEMM_EHIP, "hipGetDevice failed");
+    int chunk, nblk;
+    bucket_geometry(n, &chunk, &nblk);
+    rc = grow(&ws->perm, &ws->perm_cap, (size_t)n);
+    if (rc == QGEMM_OK) rc = grow(&ws->counts, &ws->counts_cap, (size_t)nblk * E);
+    if (rc == QGEMM_OK && ws->flag == nullptr) {
+      size_t one = 0;
+      rc = grow(&ws->flag, &one, 1);
+      if (rc == QGEMM_OK) {
+        if (hipMemset(ws->flag, 0, sizeof(int32_t)) != hipSuccess) rc = fail(QGEMM_EHIP, "hipMemset failed");
+      }
+    }
+    if (rc != QGEMM_OK) return rc;
+    ws->seq = ws->seq == 0x7fffffff ? 1 : ws->seq + 1;
+    seq = ws->seq;
+    perm = ws->perm;
+    flag = ws->flag;
+    (void)hipGetLastError();
+    rc = enqueue_bucket(token_expert_idx, expert_offsets, perm, n, E, ws->counts, flag, seq, y, N, stream);
+    if (rc != QGEMM_OK) return rc;
+  }
+  qg::TileArgs a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.y = y;
+  a.M = n;
+  a.N = N;
+  a.K = K;
+  a.perm = perm;
+  a.offsets = expert_offsets;
+  a.topk = topk;
+  a.T = T;
+  rc = (fmt == QGEMM_Q8) ? launch_moe<qg::kQ8>(a, wq, scales, E, stream)
+                         : launch_moe<qg::kQ4>(a, wq, scales, E, stream);
+  if (rc != QGEMM_OK) return rc;
+  if (validate_env()) {
+    if (hipStreamSynchronize(stream) != hipSuccess) return fail(QGEMM_EHIP, "hipStreamSynchronize failed");
+    int32_t h = 0;
+    if (hipMemcpy(&h, flag, sizeof h, hipMemcpyDeviceToHost) != hipSuccess) return fail(QGEMM_EHIP, "hipMemcpy failed");
+    if (h == seq) return fail(QGEMM_EINVAL, "token_expert_idx and expert_offsets disagree");
+  }
+  return ok();
+}
+
+int qgemm_swiglu(const float* y1, void* h, int rows, int inter, hipStream_t stream) {
+  if (rows < 0 || inter < 8 || inter % 8 != 0)
+    return fail(QGEMM_EINVAL, "rows must be >= 0 and inter a positive multiple of 8");
+  if (rows == 0) return ok();
+  if (!y1 || !h) return fail(QGEMM_EINVAL, "null pointer argument");
+  if (!aligned16(y1) || !aligned16(h)) return fail(QGEMM_EALIGN, "y1 and h must be 16-byte aligned");
+  const long groups = (long)rows * (inter / 8);
+  const long blocks = (groups + 255) / 256;
+  if (blocks > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "problem too large");
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(qg::swiglu_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, y1,
+                     static_cast<uint16_t*>(h), groups, inter);
+  const int rc = check_launch("qgemm_swiglu");
+  return rc == QGEMM_OK ? ok() : rc;
+}
+
+int qgemm_moe_combine(const float* y2, const float* route_w, float* out, int T, int topk, int N, hipStream_t stream) {
+  if (T < 0 || topk < 1 || N < 4 || N % 4 != 0)
+    return fail(QGEMM_EINVAL, "T must be >= 0, topk >= 1 and N a positive multiple of 4");
+  if (T == 0) return ok();
+  if (!y2 || !route_w || !out) return fail(QGEMM_EINVAL, "null pointer argument");
+  if (!aligned16(y2) || !aligned16(out) || !aligned16(route_w))
+    return fail(QGEMM_EALIGN, "y2, route_w and out must be 16-byte aligned");
+  const long groups = (long)T * (N / 4);
+  const long blocks = (groups + 255) / 256;
+  if (blocks > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "problem too large");
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(qg::combine_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, y2, route_w, out, groups,
+                     topk, N);
+  const int rc = check_launch("qgemm_moe_combine");
+  return rc == QGEMM_OK ? ok() : rc;
+}
+
+int qgemm_release(void) {
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  for (size_t d = 0; d < g_ws.size(); ++d) {
+    Workspace& w = g_ws[d];
+    if (!w.perm && !w.counts && !w.flag) continue;
+    (void)hipSetDevice((int)d);
+    if (w.perm) (void)hipFree(w.perm);
+    if (w.counts) (void)hipFree(w.counts);
+    if (w.flag) (void)hipFree(w.flag);
+    w = Workspace{};
+  }
+  (void)hipSetDevice(cur);
+  (void)hipGetLastError();
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,159 @@
+// Bandwidth-bound helpers around the grouped GEMM: stable bucketing of token
+// slots by expert (each active expert needs the list of tokens routed to it,
+// Section 3.1 MoE expert GEMM item), the SiLU-gated activation between the
+// gate/up and down projections (Section 3.1, fused gate/up item) and the
+// router-weighted combine of the selected experts' outputs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace qg {
+
+constexpr int kBucketThreads = 256;
+constexpr int kBadExpert = INT32_MIN;
+
+// Per-block histogram of expert ids over a chunk of `chunk` assignments.
+// counts: [gridDim.x][E]
+__global__ __launch_bounds__(kBucketThreads) void bucket_count_kernel(const int32_t* __restrict__ idx, int n,
+                                                                      int E, int chunk,
+                                                                      int32_t* __restrict__ counts) {
+  extern __shared__ int32_t hist[];
+  for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
+  __syncthreads();
+  const long base = (long)blockIdx.x * chunk;
+  for (int i = threadIdx.x; i < chunk; i += blockDim.x) {
+    const long a = base + i;
+    if (a >= n) break;
+    const int e = idx[a];
+    if (e >= 0 && e < E) atomicAdd(&hist[e], 1);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += blockDim.x) counts[(long)blockIdx.x * E + e] = hist[e];
+}
+
+// Stable scatter: perm[offsets[e] + r] = the r-th assignment (in increasing
+// order) routed to expert e. Each block places its chunk after the entries of
+// earlier blocks (prefix of `counts`), then walks the chunk in rounds of
+// blockDim assignments; inside a round, lanes with equal expert ids are
+// ranked by lane order (wave ballots) and waves are taken in order.
+// An expert whose total count disagrees with offsets (or whose segment leaves
+// [0, n)) is marked bad: its declared segment is filled with -1, its
+// assignments are skipped, the error flag receives `seq`, and if `ypoison` is
+// given the y rows of those assignments (and of out-of-range ids) become NaN.
+__global__ __launch_bounds__(kBucketThreads) void bucket_scatter_kernel(
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ offsets, int n, int E, int chunk,
+    const int32_t* __restrict__ counts, int nblk, int32_t* __restrict__ perm, int32_t* __restrict__ err_flag,
+    int seq, float* __restrict__ ypoison, int N) {
+  extern __shared__ int32_t cursor[];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < E; e += blockDim.x) {
+    const int lo = offsets[e];
+    const int hi = offsets[e + 1];
+    long c = lo;
+    long tot = 0;
+    for (int b = 0; b < nblk; ++b) {
+      const int v = counts[(long)b * E + e];
+      if (b < (int)blockIdx.x) c += v;
+      tot += v;
+    }
+    const bool bad = (lo < 0) || (hi > n) || (hi < lo) || (tot != (long)hi - lo) || (e == 0 && lo != 0);
+    cursor[e] = bad ? kBadExpert : (int)c;
+    if (bad) {
+      if (blockIdx.x == 0) {
+        err_flag[0] = seq;
+        const int s0 = lo < 0 ? 0 : lo;
+        const int s1 = hi > n ? n : hi;
+        for (int p = s0; p < s1; ++p) perm[p] = -1;
+      }
+    }
+  }
+  __syncthreads();
+
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int nwaves = blockDim.x >> 6;
+  int nbits = 0;
+  while ((1 << nbits) < E) ++nbits;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const long base = (long)blockIdx.x * chunk;
+  for (int r0 = 0; r0 < chunk; r0 += blockDim.x) {
+    const long a = base + r0 + tid;
+    const bool valid = (r0 + tid < chunk) && (a < n);
+    const int e = valid ? idx[a] : -1;
+    const bool inrange = valid && e >= 0 && e < E;
+    if (valid && !inrange) {
+      err_flag[0] = seq;
+      if (ypoison != nullptr)
+        for (int j = 0; j < N; ++j) ypoison[a * (long)N + j] = __builtin_nanf("");
+    }
+    uint64_t same = __ballot(inrange);
+    for (int b = 0; b < nbits; ++b) {
+      const bool bit = inrange && ((e >> b) & 1);
+      const uint64_t m = __ballot(bit);
+      same &= bit ? m : ~m;
+    }
+    const int rank = __popcll(same & lt_mask);
+    const int cnt = __popcll(same);
+    for (int w = 0; w < nwaves; ++w) {
+      if (wave == w && inrange) {
+        const int cb = cursor[e];
+        if (cb != kBadExpert) {
+          perm[cb + rank] = (int32_t)a;
+        } else if (ypoison != nullptr) {
+          for (int j = 0; j < N; ++j) ypoison[a * (long)N + j] = __builtin_nanf("");
+        }
+        if (rank == 0 && cb != kBadExpert) cursor[e] = cb + cnt;
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// h[r][i] = bf16(silu(g) * u), g = y1[r][i], u = y1[r][inter + i]; 8 outputs per thread.
+__global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ y1, uint16_t* __restrict__ h,
+                                                     long groups, int inter) {
+  const long gid = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= groups) return;
+  const int per_row = inter >> 3;
+  const long r = gid / per_row;
+  const int i0 = (int)(gid - r * per_row) * 8;
+  const float* grow = y1 + r * (2L * inter) + i0;
+  const float4 g0 = *reinterpret_cast<const float4*>(grow);
+  const float4 g1 = *reinterpret_cast<const float4*>(grow + 4);
+  const float4 u0 = *reinterpret_cast<const float4*>(grow + inter);
+  const float4 u1 = *reinterpret_cast<const float4*>(grow + inter + 4);
+  const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+  const float u[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float a0 = g[2 * i] / (1.0f + __expf(-g[2 * i])) * u[2 * i];
+    const float a1 = g[2 * i + 1] / (1.0f + __expf(-g[2 * i + 1])) * u[2 * i + 1];
+    o[i] = pack_bf16x2(a0, a1);
+  }
+  *reinterpret_cast<uint4*>(h + r * inter + i0) = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+// out[t][n] = sum_j w[t*topk+j] * y2[t*topk+j][n], fp32 fused multiply-add in increasing j.
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ y2, const float* __restrict__ w,
+                                                      float* __restrict__ out, long groups, int topk, int N) {
+  const long gid = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= groups) return;
+  const int per_row = N >> 2;
+  const long t = gid / per_row;
+  const int n0 = (int)(gid - t * per_row) * 4;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int j = 0; j < topk; ++j) {
+    const long a = t * topk + j;
+    const float wj = w[a];
+    const float4 v = *reinterpret_cast<const float4*>(y2 + a * N + n0);
+    acc.x = __builtin_fmaf(wj, v.x, acc.x);
+    acc.y = __builtin_fmaf(wj, v.y, acc.y);
+    acc.z = __builtin_fmaf(wj, v.z, acc.z);
+    acc.w = __builtin_fmaf(wj, v.w, acc.w);
+  }
+  *reinterpret_cast<float4*>(out + t * N + n0) = acc;
+}
+
+}  // namespace qg

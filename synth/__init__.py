@@ -47,8 +47,9 @@ def rng_for(seed: int, *stream: int) -> np.random.Generator:
 def bf16_bits(a) -> np.ndarray:
     """Round values to bf16 (via float32, round-to-nearest-even) and return uint16 bits."""
     f = np.ascontiguousarray(np.asarray(a, dtype=np.float32))
-    u = f.view(np.uint32).astype(np.uint64)
-    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    u = f.view(np.uint32)
+    # finite inputs have u <= 0xFF7FFFFF, so adding at most 0x8000 cannot wrap
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return r.astype(np.uint16)
 
 
@@ -57,9 +58,9 @@ def pack_nibbles(u: np.ndarray) -> np.ndarray:
     u = np.asarray(u)
     if u.shape[-1] % 2:
         raise ValueError("K must be even to pack nibbles")
-    if u.min(initial=0) < 0 or u.max(initial=0) > 15:
+    if u.size and (u.min() < 0 or u.max() > 15):
         raise ValueError("nibbles must lie in [0, 15]")
-    u = u.astype(np.uint8)
+    u = u.astype(np.uint8, copy=False)
     return (u[..., 0::2] | (u[..., 1::2] << 4)).astype(np.uint8)
 
 
@@ -80,21 +81,21 @@ class QWeight:
     K: int
     wq: np.ndarray          # int8 [N][K] (Q8) or uint8 [N][K/2] (Q4)
     scales: np.ndarray      # float16 [N][K/32]
-    q: np.ndarray           # int16 [N][K], signed values encoded by wq
+    q: np.ndarray | None    # int16 [N][K], signed values encoded by wq (None when not kept)
 
 
 def make_qweight(rng: np.random.Generator, N: int, K: int, fmt: int,
-                 scale_range=None) -> QWeight:
+                 scale_range=None, keep_q: bool = True) -> QWeight:
     if K % QBLOCK:
         raise ValueError("K must be a multiple of 32")
     lo, hi = scale_range or SCALE_RANGE[fmt]
     if fmt == FMT_Q8:
-        q = rng.integers(-127, 128, size=(N, K), dtype=np.int16)
-        wq = q.astype(np.int8)
+        wq = rng.integers(-127, 128, size=(N, K), dtype=np.int8)
+        q = wq.astype(np.int16) if keep_q else None
     elif fmt == FMT_Q4:
-        u = rng.integers(0, 16, size=(N, K), dtype=np.int16)
+        u = rng.integers(0, 16, size=(N, K), dtype=np.uint8)
         wq = pack_nibbles(u)
-        q = (u - 8).astype(np.int16)
+        q = (u.astype(np.int16) - 8) if keep_q else None
     else:
         raise ValueError(f"unknown fmt {fmt}")
     scales = rng.uniform(lo, hi, size=(N, K // QBLOCK)).astype(np.float16)
@@ -119,7 +120,17 @@ def qweight_from_q(q: np.ndarray, scales: np.ndarray, fmt: int) -> QWeight:
 
 def make_x(rng: np.random.Generator, M: int, K: int) -> np.ndarray:
     """Activations ~ N(0, 1) rounded to bf16; returns uint16 bits ``[M][K]``."""
-    return bf16_bits(rng.standard_normal((M, K)))
+    return bf16_bits(rng.standard_normal((M, K), dtype=np.float32))
+
+
+def make_x_product(rng: np.random.Generator, M: int, K: int) -> np.ndarray:
+    """Heavy-tailed activations: the product of two independent N(0, 1) draws, rounded to bf16.
+
+    Stand-in input of the MoE down projection, whose activations are products of
+    two roughly normal projections."""
+    a = rng.standard_normal((M, K), dtype=np.float32)
+    b = rng.standard_normal((M, K), dtype=np.float32)
+    return bf16_bits(a * b)
 
 
 # ---------------------------------------------------------------------------
@@ -234,8 +245,8 @@ def moe_case(name: str, fmt: int, T: int, E: int, topk: int, hidden: int, inter:
     r = moe_routing(T, E, topk, skew, seed, stream)
     rg = rng_for(seed, *stream, 2)
     rd = rng_for(seed, *stream, 3)
-    wgu = [make_qweight(rg, 2 * inter, hidden, fmt) for _ in range(E)]
-    wd = [make_qweight(rd, hidden, inter, fmt) for _ in range(E)]
+    wgu = [make_qweight(rg, 2 * inter, hidden, fmt, keep_q=False) for _ in range(E)]
+    wd = [make_qweight(rd, hidden, inter, fmt, keep_q=False) for _ in range(E)]
     return MoECase(name, fmt, T, E, topk, hidden, inter, x, r, wgu, wd)
 
 

@@ -1,0 +1,108 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the header declares, and
+rejects bad arguments on the host before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qgemm.h")
+
+
+@pytest.fixture(scope="module")
+def qmod():
+    import paper_2607_19438_amd as q
+    if not os.path.exists(q.lib_path()):
+        from paper_2607_19438_amd import build
+        build.build()
+    return q
+
+
+def header_prototypes():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    protos = {}
+    for m in re.finditer(r"\b(?:int|const char\s*\*|void)\s+(qgemm_\w+)\s*\(([^)]*)\)\s*;", text):
+        args = m.group(2).strip()
+        n = 0 if args in ("", "void") else args.count(",") + 1
+        protos[m.group(1)] = n
+    return protos
+
+
+def test_header_declares_the_boundary():
+    p = header_prototypes()
+    for name in ("qgemm_dense", "qgemm_moe", "qgemm_moe_bucket", "qgemm_moe_grouped", "qgemm_swiglu",
+                 "qgemm_moe_combine", "qgemm_last_error", "qgemm_release", "qgemm_version"):
+        assert name in p
+
+
+def test_library_exports_every_header_symbol(qmod):
+    lib = ctypes.CDLL(qmod.lib_path())
+    for name, nargs in header_prototypes().items():
+        assert hasattr(lib, name), name
+        assert name in qmod.EXPORTS, name
+        assert len(qmod.EXPORTS[name][1]) == nargs, name
+    assert set(qmod.EXPORTS) == set(header_prototypes())
+
+
+def test_version_and_last_error(qmod):
+    assert qmod.version() >> 16 == 1
+    assert isinstance(qmod.last_error(), str)
+
+
+@pytest.mark.parametrize("args,code,msg", [
+    ((0, 0, 0, 0, 4, 4, 40, 0), -1, "multiple of 32"),
+    ((0, 0, 0, 0, 4, 4, 0, 0), -1, "multiple of 32"),
+    ((0, 0, 0, 0, 4, 0, 64, 0), -1, "N must be"),
+    ((0, 0, 0, 0, -1, 4, 64, 0), -1, "M must be"),
+    ((0, 0, 0, 0, 4, 4, 64, 7), -1, "format"),
+    ((0, 0, 0, 0, 4, 4, 64, 0), -1, "null pointer"),
+    ((16, 32, 2, 8, 4, 4, 64, 1), -2, "aligned"),
+    ((16, 32, 3, 32, 4, 4, 64, 1), -2, "aligned"),
+    ((0, 0, 0, 0, 0, 4, 64, 0), 0, ""),
+    ((16, 16, 16, 16, 1 << 20, 1 << 12, 1 << 12, 0), -3, "2^31"),
+])
+def test_dense_host_validation(qmod, args, code, msg):
+    lib = qmod.lib()
+    rc = lib.qgemm_dense(*args, None)
+    assert rc == code
+    assert msg in qmod.last_error()
+
+
+def test_moe_host_validation(qmod):
+    lib = qmod.lib()
+    ptrs = (ctypes.c_void_p * 4)(16, 32, 48, 64)
+    bad = (ctypes.c_void_p * 4)(16, 32, 40, 64)
+    assert lib.qgemm_moe(16, 16, 16, ptrs, ptrs, 16, 4, 4, 5, 128, 64, 0, None) == -1      # topk > E
+    assert lib.qgemm_moe(16, 16, 16, ptrs, ptrs, 16, 4, 0, 1, 128, 64, 0, None) == -1      # E < 1
+    assert lib.qgemm_moe(16, 16, 16, ptrs, ptrs, 16, 4, 5000, 1, 128, 64, 0, None) == -3   # E too large
+    assert lib.qgemm_moe(16, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 128, 33, 0, None) == -1      # K % 32
+    assert lib.qgemm_moe(16, 16, 16, bad, ptrs, 16, 4, 4, 2, 128, 64, 0, None) == -2       # expert 2 misaligned
+    assert "expert 2" in qmod.last_error()
+    assert lib.qgemm_moe(16, 16, 16, ptrs, ptrs, 16, 0, 4, 2, 128, 64, 0, None) == 0       # T == 0
+    assert lib.qgemm_moe(0, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 128, 64, 0, None) == -1       # null x
+    assert lib.qgemm_moe_grouped(16, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 128, 64, 9, None) == -1
+    assert lib.qgemm_moe_bucket(16, 16, 16, -1, 4, None) == -1
+    assert lib.qgemm_moe_bucket(16, 16, 16, 0, 4, None) == 0
+    assert lib.qgemm_swiglu(16, 16, 4, 12, None) == -1
+    assert lib.qgemm_swiglu(16, 16, 0, 16, None) == 0
+    assert lib.qgemm_moe_combine(16, 16, 16, 4, 2, 6, None) == -1
+    assert lib.qgemm_moe_combine(16, 16, 16, 0, 2, 8, None) == 0
+
+
+def test_product_never_imports_oracle():
+    pkg = os.path.join(ROOT, "paper_2607_19438_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".hpp", ".cpp", ".h")):
+                src = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"\b(import|from)\s+(oracle|synth)\b", src), f
+                assert "oracle/" not in src and "qgemm_oracle" not in src, f
+
+
+def test_missing_library_fails_loudly(qmod, monkeypatch):
+    monkeypatch.setattr(qmod, "_lib", None)
+    monkeypatch.setattr(qmod, "_LIB_PATH", "/nonexistent/libqgemm.so")
+    with pytest.raises(qmod.QGemmError):
+        qmod.lib()

@@ -191,3 +191,28 @@ def test_rejects_bad_shapes():
         oracle.dequant(np.zeros((2, 40), np.int8), np.ones((2, 1), np.float16), synth.FMT_Q8, 40)
     with pytest.raises(ValueError):
         oracle.decode_q(np.zeros((2, 16), np.uint8), synth.FMT_Q4, 64)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_bf16_weight_variant_rounds_each_exact_weight_once(fmt):
+    """bf16_weights=True: each q*s rounded to nearest bf16 (ties even), checked with exact rationals."""
+    from test_oracle_moe import round_bf16_scalar
+    rng = synth.rng_for(31, fmt)
+    M, N, K = 3, 4, 64
+    x = synth.make_x(rng, M, K)
+    w = synth.make_qweight(rng, N, K, fmt)
+    wr = oracle.dequant(w.wq, w.scales, fmt, K, bf16_weights=True)
+    for n in range(N):
+        for k in range(K):
+            exact = float(w.scales[n, k // 32]) * int(w.q[n, k])      # exact in float64
+            assert wr[n, k] == round_bf16_scalar(exact)
+    y, b = oracle.dense(x, w.wq, w.scales, fmt, bf16_weights=True)
+    for m in range(M):
+        for n in range(N):
+            terms = [Fraction(bf16_value_struct(x[m, k])) * Fraction(round_bf16_scalar(
+                float(w.scales[n, k // 32]) * int(w.q[n, k]))) for k in range(K)]
+            ex = sum(terms)
+            bx = sum(abs(t) for t in terms)
+            assert abs(Fraction(y[m, n]) - ex) <= K * 2.0 ** -52 * bx
+    # and the rounding really moves weights: the variant differs from the exact weights
+    assert np.any(wr != oracle.dequant(w.wq, w.scales, fmt, K))

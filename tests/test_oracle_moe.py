@@ -210,3 +210,40 @@ def test_combine_closed_forms():
     b = np.abs(y2)
     _, bnd = oracle.combine(y2, -w2, topk, b)
     np.testing.assert_allclose(bnd, (b.reshape(T, topk, N) * np.array([0.25, 0.25, 0.5])[None, :, None]).sum(1))
+
+
+def test_silu_lipschitz_constant_bounds_derivative():
+    z = np.linspace(-40, 40, 800001)
+    d = np.gradient(oracle.silu(z), z)
+    assert np.max(np.abs(d)) <= oracle.SILU_LIPSCHITZ
+    assert np.max(np.abs(d)) > oracle.SILU_LIPSCHITZ - 1e-3      # and it is tight
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_ffn_tolerance_covers_perturbed_chains(fmt):
+    """Perturb each GEMM's output within the bar (worst-case signs and random), recompute the rest
+    of the chain exactly as the oracle does, and check the FFN output stays within the tolerance."""
+    T, E, topk, hidden, inter = 24, 4, 2, 64, 32
+    rng = synth.rng_for(40, fmt)
+    x = synth.make_x(rng, T, hidden)
+    r = synth.make_routing(rng, T, E, topk)
+    wgu = [synth.make_qweight(rng, 2 * inter, hidden, fmt) for _ in range(E)]
+    wd = [synth.make_qweight(rng, hidden, inter, fmt) for _ in range(E)]
+    args = (x, r.token_expert_idx, r.expert_offsets, r.route_w, [w.wq for w in wgu], [w.scales for w in wgu],
+            [w.wq for w in wd], [w.scales for w in wd], topk, inter, fmt)
+    res = oracle.moe_ffn(*args)
+    tol = oracle.ffn_out_tolerance(res, r.token_expert_idx, r.route_w, [w.wq for w in wd], [w.scales for w in wd],
+                                   topk, inter, fmt)
+    worst = 0.0
+    for trial in range(40):
+        rr = synth.rng_for(41, trial)
+        s1 = rr.choice([-1.0, 1.0], size=res["y1"].shape) if trial % 2 else rr.uniform(-1, 1, res["y1"].shape)
+        y1p = res["y1"] + s1 * (oracle.TOL_REL * res["bound1"] + oracle.TOL_ABS)
+        _, hb = oracle.swiglu(y1p, inter)
+        y2p, _ = oracle.moe(hb, r.token_expert_idx, r.expert_offsets, [w.wq for w in wd], [w.scales for w in wd], 1, fmt)
+        s2 = rr.choice([-1.0, 1.0], size=y2p.shape)
+        y2p = y2p + s2 * (oracle.TOL_REL * res["bound2"] + oracle.TOL_ABS)
+        outp, _ = oracle.combine(y2p, r.route_w, topk)
+        worst = max(worst, float(np.max(np.abs(outp - res["out"]) / tol)))
+    assert worst <= 1.0
+    assert worst > 0.05          # the tolerance is not vacuous
