@@ -95,8 +95,8 @@ def build_parts(torch, q, synth, only):
         p.sgu = torch.from_numpy(np.stack([w.scales for w in case.w_gate_up])).to(dev)
         p.wd = torch.from_numpy(np.stack([w.wq for w in case.w_down])).to(dev)
         p.sd = torch.from_numpy(np.stack([w.scales for w in case.w_down])).to(dev)
-        p.wgu_l, p.sgu_l = list(p.wgu.unbind(0)), list(p.sgu.unbind(0))
-        p.wd_l, p.sd_l = list(p.wd.unbind(0)), list(p.sd.unbind(0))
+        p.tgu = q.ExpertTable(p.wgu, p.sgu, case.fmt)
+        p.td = q.ExpertTable(p.wd, p.sd, case.fmt)
         p.perm = torch.empty((A,), dtype=torch.int32, device=dev)
         p.y1 = torch.empty((A, 2 * case.inter), dtype=torch.float32, device=dev)
         p.h = torch.empty((A, case.inter), dtype=torch.bfloat16, device=dev)
@@ -117,10 +117,10 @@ def run_part(q, p, timer=None):
     c = p.case
     q.moe_bucket(p.idx, p.off, out=p.perm)
     with timer(p.name + ":gate_up"):
-        q.moe_grouped(p.x, p.perm, p.off, p.wgu_l, p.sgu_l, c.topk, c.fmt, out=p.y1)
+        q.moe_grouped(p.x, p.perm, p.off, p.tgu, None, c.topk, c.fmt, out=p.y1)
     q.swiglu(p.y1, out=p.h)
     with timer(p.name + ":down"):
-        q.moe_grouped(p.h, p.perm, p.off, p.wd_l, p.sd_l, 1, c.fmt, out=p.y2)
+        q.moe_grouped(p.h, p.perm, p.off, p.td, None, 1, c.fmt, out=p.y2)
     q.moe_combine(p.y2, p.rw, c.topk, out=p.out)
 
 
@@ -231,9 +231,10 @@ def main():
     for _ in range(args.steps):
         for p in parts:
             run_part(q, p, timer)
+    enq = time.perf_counter() - t0
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    log(f"timed {args.steps} steps in {wall:.3f} s")
+    log(f"timed {args.steps} steps in {wall:.3f} s (host enqueue {enq / args.steps * 1e3:.3f} ms/step)")
     ms_per_step = wall / args.steps * 1e3
     flops_step = sum(p.flops for p in parts)
     value = flops_step / (wall / args.steps) / 1e12

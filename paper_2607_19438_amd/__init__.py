@@ -16,7 +16,7 @@ import os
 import torch  # imported before the library so that both share one HIP runtime
 
 __all__ = ["Q8", "Q4", "QGemmError", "lib", "lib_path", "dense", "moe", "moe_bucket", "moe_grouped",
-           "swiglu", "moe_combine", "last_error", "release", "version", "EXPORTS"]
+           "swiglu", "moe_combine", "last_error", "release", "version", "EXPORTS", "ExpertTable"]
 
 Q8 = 0
 Q4 = 1
@@ -127,8 +127,41 @@ def dense(x: torch.Tensor, wq: torch.Tensor, scales: torch.Tensor, fmt: int, out
     return out
 
 
-def _expert_tables(wq, scales, E):
+class ExpertTable:
+    """Validated per-expert weights with their host pointer arrays, built once and reused.
+
+    ``wq`` / ``scales``: lists of E tensors or stacked ``[E, N, K']`` / ``[E, N, K/32]`` tensors.
+    """
+
+    def __init__(self, wq, scales, fmt: int):
+        if isinstance(wq, torch.Tensor):
+            wq = list(wq.unbind(0))
+        if isinstance(scales, torch.Tensor):
+            scales = list(scales.unbind(0))
+        if len(wq) != len(scales) or not wq:
+            raise ValueError("need one weight and one scale tensor per expert")
+        for t in wq:
+            _need(t, "wq[e]", _W_DTYPES, 2)
+        for t in scales:
+            _need(t, "scales[e]", (torch.float16,), 2)
+        self.E = len(wq)
+        self.N = wq[0].shape[0]
+        self.K = _wshape_k(wq[0], fmt)
+        self.fmt = fmt
+        if any(w.shape[0] != self.N or _wshape_k(w, fmt) != self.K for w in wq) or any(
+                s.shape != (self.N, self.K // 32) for s in scales):
+            raise ValueError("expert weights disagree on N or K")
+        self.wq, self.scales = wq, scales          # keep the tensors alive
+        self.wp = (ctypes.c_void_p * self.E)(*[t.data_ptr() for t in wq])
+        self.sp = (ctypes.c_void_p * self.E)(*[t.data_ptr() for t in scales])
+
+
+def _expert_tables(wq, scales, E, fmt=None):
     """Host arrays of per-expert device pointers from lists or stacked [E, ...] tensors."""
+    if isinstance(wq, ExpertTable):
+        if wq.E != E:
+            raise ValueError("expert table has the wrong number of experts")
+        return wq.wq, wq.scales, wq.wp, wq.sp
     if isinstance(wq, torch.Tensor):
         wq = list(wq.unbind(0))
     if isinstance(scales, torch.Tensor):
@@ -145,7 +178,9 @@ def _expert_tables(wq, scales, E):
 
 
 def moe(x, token_expert_idx, expert_offsets, wq, scales, topk: int, fmt: int, out=None):
-    """MoE expert GEMM over token slots (``qgemm_moe``): ``y[T*topk][N]`` fp32 in slot order."""
+    """MoE expert GEMM over token slots (``qgemm_moe``): ``y[T*topk][N]`` fp32 in slot order.
+
+    ``wq`` may be an ExpertTable (then ``scales`` is ignored)."""
     _need(x, "x", (torch.bfloat16,), 2)
     _need(token_expert_idx, "token_expert_idx", (torch.int32,), 1)
     _need(expert_offsets, "expert_offsets", (torch.int32,), 1)
@@ -180,7 +215,7 @@ def moe_bucket(token_expert_idx, expert_offsets, out=None):
 
 
 def moe_grouped(x, perm, expert_offsets, wq, scales, topk: int, fmt: int, out=None):
-    """Grouped GEMM from an existing bucketing (``qgemm_moe_grouped``)."""
+    """Grouped GEMM from an existing bucketing (``qgemm_moe_grouped``); ``wq`` may be an ExpertTable."""
     _need(x, "x", (torch.bfloat16,), 2)
     _need(perm, "perm", (torch.int32,), 1)
     _need(expert_offsets, "expert_offsets", (torch.int32,), 1)

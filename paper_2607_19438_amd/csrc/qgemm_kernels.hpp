@@ -19,6 +19,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
 constexpr int kQ8 = 0;
 constexpr int kQ4 = 1;
@@ -40,10 +42,12 @@ __device__ __forceinline__ float fp16_to_f32(uint16_t h) {
 }
 
 // Byte offset of 16-byte chunk `c` (0..7) of row `r` in a [rows][64] bf16 LDS tile.
-// Chunks are XOR-swizzled by the row so that 32 lanes reading the same chunk
-// column of 32 consecutive rows spread over all LDS banks.
+// LDS has 64 four-byte banks (256 bytes), i.e. two 128-byte tile rows. Chunks are
+// XOR-swizzled by the row pair (r >> 1), so any 16 consecutive rows read at the
+// same logical chunk land on 16 distinct 16-byte bank groups (the 16 lanes that
+// one ds_read_b128 phase serves), and 4 rows x 4 even (or odd) chunks do too.
 __device__ __forceinline__ int lds_chunk(int r, int c) {
-  return r * kRowBytes + ((c ^ (r & 7)) << 4);
+  return r * kRowBytes + ((c ^ ((r >> 1) & 7)) << 4);
 }
 
 // 16 int8 weights (one 16-byte load) -> 16 bf16 = w * s, as 8 packed dwords.
@@ -74,6 +78,41 @@ __device__ __forceinline__ void dequant_q4x32(const uint4 w, float s, uint32_t o
       out[4 * i + b] = pack_bf16x2(__builtin_fmaf(lo, s, o), __builtin_fmaf(hi, s, o));
     }
   }
+}
+
+// One 16-byte LDS unit of dequantised weights = 8 bf16.
+// Q8: two dwords of int8 (8 weights) with scale s.
+__device__ __forceinline__ u32x4 dequant_q8_unit(uint32_t d0, uint32_t d1, float s) {
+  const float f0 = (float)(int8_t)(d0), f1 = (float)(int8_t)(d0 >> 8);
+  const float f2 = (float)(int8_t)(d0 >> 16), f3 = (float)(int8_t)(d0 >> 24);
+  const float f4 = (float)(int8_t)(d1), f5 = (float)(int8_t)(d1 >> 8);
+  const float f6 = (float)(int8_t)(d1 >> 16), f7 = (float)(int8_t)(d1 >> 24);
+  return u32x4{pack_bf16x2(f0 * s, f1 * s), pack_bf16x2(f2 * s, f3 * s), pack_bf16x2(f4 * s, f5 * s),
+               pack_bf16x2(f6 * s, f7 * s)};
+}
+
+// Q4: one dword of 8 nibbles (element 2b in the low nibble of byte b, 2b+1 in the
+// high nibble). The low nibbles are masked in place (u), the high nibbles masked in
+// place too (16 u), so each converts with one byte-select cvt; s16 = s / 16 is exact.
+__device__ __forceinline__ u32x4 dequant_q4_unit(uint32_t d, float s, float s16, float off) {
+  uint32_t lo = d & 0x0F0F0F0Fu;
+  uint32_t hi = d & 0xF0F0F0F0u;
+  asm volatile("" : "+v"(lo), "+v"(hi));   // keep the byte-select conversions below
+  const float l0 = (float)(lo & 0xFFu), l1 = (float)((lo >> 8) & 0xFFu);
+  const float l2 = (float)((lo >> 16) & 0xFFu), l3 = (float)(lo >> 24);
+  const float h0 = (float)(hi & 0xFFu), h1 = (float)((hi >> 8) & 0xFFu);
+  const float h2 = (float)((hi >> 16) & 0xFFu), h3 = (float)(hi >> 24);
+  return u32x4{pack_bf16x2(__builtin_fmaf(l0, s, off), __builtin_fmaf(h0, s16, off)),
+               pack_bf16x2(__builtin_fmaf(l1, s, off), __builtin_fmaf(h1, s16, off)),
+               pack_bf16x2(__builtin_fmaf(l2, s, off), __builtin_fmaf(h2, s16, off)),
+               pack_bf16x2(__builtin_fmaf(l3, s, off), __builtin_fmaf(h3, s16, off))};
+}
+
+// s_waitcnt vmcnt(n) expcnt(7) lgkmcnt(0) (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
 }
 
 // ---------------------------------------------------------------------------
@@ -114,120 +153,166 @@ __device__ __forceinline__ int xcd_tile(int bid, int ntiles) {
 template <int FMT, int BM, int BN, int WM, int WN, bool MOE>
 struct TileKernel {
   static constexpr int kThreads = WM * WN * 64;
+  static constexpr int kWaves = WM * WN;
   static constexpr int kWTM = BM / WM;        // rows per wave
   static constexpr int kWTN = BN / WN;        // cols per wave
   static constexpr int kTM = kWTM / 32;       // 32x32 MFMA blocks per wave (M)
   static constexpr int kTN = kWTN / 32;       // (N)
-  static constexpr int kXChunks = BM * 8 / kThreads;            // 16-byte x chunks per thread per K step
+  static constexpr int kXLoads = BM / 8 / kWaves;               // 1 KiB LDS-DMA loads (8 rows) per wave per K step
   static constexpr int kWChunkElems = (FMT == kQ8) ? 16 : 32;   // weights per 16-byte load
   static constexpr int kWChunksPerRow = kBK / kWChunkElems;     // 4 (Q8) or 2 (Q4)
+  static constexpr int kWStepBytes = (FMT == kQ8) ? kBK : kBK / 2;   // packed bytes of one row per K step
   static constexpr int kWChunks = BN * kWChunksPerRow / kThreads;
-  static constexpr int kTileBytes = (BM + BN) * kRowBytes;
-  static constexpr int kLdsBytes = 2 * kTileBytes;
-  static_assert(kXChunks * kThreads == BM * 8, "x tile must split evenly");
+  static constexpr int kXTileBytes = BM * kRowBytes;
+  static constexpr int kStageBytes = (BM + BN) * kRowBytes;
+  static constexpr int kLdsBytes = 2 * kStageBytes;
+  static_assert(kXLoads * kWaves * 8 == BM, "x tile must split into 8-row groups per wave");
   static_assert(kWChunks * kThreads == BN * kWChunksPerRow, "w tile must split evenly");
   static_assert(kTM >= 1 && kTN >= 1, "wave tile must hold a 32x32 block");
 };
 
-template <int FMT, int BM, int BN, int WM, int WN, bool MOE>
+typedef __attribute__((address_space(3))) char lds_char;
+
+constexpr uint32_t kBufferFlags = 0x00020000;   // raw buffer, 32-bit dwords (gfx9 family)
+constexpr uint32_t kOOB = 0xFFFFFFF0u;          // offset past every buffer: loads return 0
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferFlags);
+}
+
+#define QG_SG(mask, n) __builtin_amdgcn_sched_group_barrier((mask), (n), 0)
+constexpr int kSchedMFMA = 0x008;
+constexpr int kSchedVALU = 0x002;
+constexpr int kSchedDSRead = 0x100;
+constexpr int kSchedDSWrite = 0x200;
+
+// One output tile: rows [m0, m0 + rows_valid) of x (dense) or the gathered rows
+// s_xrow[] (MoE), columns [n0, n0 + BN) of W.
+//
+// Pipeline per 64-wide K step kt (two LDS stages, two weight register sets):
+//   issue activation DMA for step kt+1 into stage (kt+1)&1     (buffer_load ... lds)
+//   issue packed-weight + scale loads for step kt+2            (registers)
+//   four K16 sub-steps over stage kt&1: MFMAs, with the next sub-step's LDS
+//   fragments and one quarter of step kt+1's dequantisation (into stage
+//   (kt+1)&1) interleaved between them
+//   wait for the activation DMA and the LDS writes, then barrier
+// FULL: every row of the tile is valid, so no MFMA is skipped (branch-free body).
+template <int FMT, int BM, int BN, int WM, int WN, bool MOE, bool FULL>
 __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __restrict__ wq,
                                           const uint16_t* __restrict__ sc, int m0, int n0,
                                           int rows_valid, const int* __restrict__ s_xrow,
-                                          const int* __restrict__ s_yrow, char* __restrict__ lds) {
+                                          const int* __restrict__ s_yrow, char* __restrict__ lds_generic) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, MOE>;
+  constexpr int kUnitsPerChunk = (FMT == kQ8) ? 2 : 4;        // 16-byte LDS writes per 16-byte load
+  constexpr int kUnits = KT::kWChunks * kUnitsPerChunk;        // per thread per K step
+  static_assert(kUnits % 4 == 0, "units must spread evenly over the four K16 sub-steps");
+  constexpr int kUnitsPerKK = kUnits / 4;
+  constexpr int kMfmaPerKK = KT::kTM * KT::kTN;
+  constexpr int kValuPerUnit = (FMT == kQ8) ? 20 : 22;
+  constexpr int kValuPerMfma = (kUnitsPerKK * kValuPerUnit + 4 + kMfmaPerKK - 1) / kMfmaPerKK;
+
+  lds_char* lds = (lds_char*)lds_generic;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN;
   const int wn = wave % WN;
   const int K = a.K;
   const int N = a.N;
   const int nk = (K + kBK - 1) / kBK;
-  const int kblocks = K >> 5;
-  const size_t wrow_bytes = (FMT == kQ8) ? (size_t)K : (size_t)(K >> 1);
+  const uint32_t kblocks = (uint32_t)K >> 5;
+  const uint32_t wrow_bytes = (FMT == kQ8) ? (uint32_t)K : (uint32_t)K >> 1;
+  const int n_valid = min(BN, N - n0);
 
-  // --- per-thread x rows (fixed across the K loop) ---
-  const uint16_t* xrow[KT::kXChunks];
-  int xc[KT::kXChunks];
+  // --- activation DMA: this lane fetches logical chunk dma_c[j] of row (8 g + lane / 8) ---
+  __amdgpu_buffer_rsrc_t xr;
+  uint32_t xoff[KT::kXLoads];
+  int dma_c[KT::kXLoads];
 #pragma unroll
-  for (int i = 0; i < KT::kXChunks; ++i) {
-    const int q = tid + i * KT::kThreads;
-    const int r = q >> 3;
-    xc[i] = q & 7;
-    int src = -1;
-    if (r < rows_valid) src = MOE ? s_xrow[r] : (m0 + r);
-    xrow[i] = (src >= 0) ? a.x + (size_t)src * K : nullptr;
+  for (int j = 0; j < KT::kXLoads; ++j) {
+    const int r = (wave * KT::kXLoads + j) * 8 + (lane >> 3);
+    dma_c[j] = (lane & 7) ^ ((r >> 1) & 7);     // the chunk that lds_chunk(r, .) places at slot lane & 7
   }
-  // --- per-thread weight rows ---
-  const uint8_t* wrow[KT::kWChunks];
-  const uint16_t* srow[KT::kWChunks];
-  int wc[KT::kWChunks];
+  if constexpr (MOE) {
+    xr = make_rsrc(a.x, (uint32_t)a.T * (uint32_t)K * 2u);
+#pragma unroll
+    for (int j = 0; j < KT::kXLoads; ++j) {
+      const int r = (wave * KT::kXLoads + j) * 8 + (lane >> 3);
+      const int src = (r < rows_valid) ? s_xrow[r] : -1;
+      xoff[j] = (src >= 0) ? (uint32_t)src * (uint32_t)K * 2u + (uint32_t)dma_c[j] * 16u : kOOB;
+    }
+  } else {
+    xr = make_rsrc(a.x + (size_t)m0 * K, (uint32_t)rows_valid * (uint32_t)K * 2u);
+#pragma unroll
+    for (int j = 0; j < KT::kXLoads; ++j) {
+      const int r = (wave * KT::kXLoads + j) * 8 + (lane >> 3);
+      xoff[j] = (uint32_t)r * (uint32_t)K * 2u + (uint32_t)dma_c[j] * 16u;
+    }
+  }
+  // --- weight / scale offsets of this thread's chunks ---
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(wq + (size_t)n0 * wrow_bytes, (uint32_t)n_valid * wrow_bytes);
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(sc + (size_t)n0 * kblocks, (uint32_t)n_valid * kblocks * 2u);
+  uint32_t woff[KT::kWChunks];
+  uint32_t soff[KT::kWChunks];
+  int lds_w[KT::kWChunks][kUnitsPerChunk];   // LDS byte offset (within the W tile) of each unit
+  int wcol[KT::kWChunks];
 #pragma unroll
   for (int i = 0; i < KT::kWChunks; ++i) {
     const int q = tid + i * KT::kThreads;
     const int r = q / KT::kWChunksPerRow;
-    wc[i] = q % KT::kWChunksPerRow;
-    const int n = n0 + r;
-    wrow[i] = (n < N) ? wq + (size_t)n * wrow_bytes : nullptr;
-    srow[i] = (n < N) ? sc + (size_t)n * kblocks : nullptr;
+    const int c = q % KT::kWChunksPerRow;
+    wcol[i] = c;
+    woff[i] = (uint32_t)r * wrow_bytes + (uint32_t)c * 16u;
+    soff[i] = ((uint32_t)r * kblocks + (uint32_t)(c * KT::kWChunkElems / 32)) * 2u;
+#pragma unroll
+    for (int u = 0; u < kUnitsPerChunk; ++u) lds_w[i][u] = lds_chunk(r, c * kUnitsPerChunk + u);
   }
 
-  uint4 xr[KT::kXChunks];
-  uint4 wr[KT::kWChunks];
-  float sr[KT::kWChunks];
-
-  auto load_step = [&](int kt) {
-    const int k0 = kt * kBK;
+  auto issue_x = [&](int kt, int stage) {
+    const uint32_t kbyte = (uint32_t)kt * (uint32_t)kRowBytes;
+    const bool tail = (kt + 1) * kBK > K;
 #pragma unroll
-    for (int i = 0; i < KT::kXChunks; ++i) {
-      const int k = k0 + xc[i] * 8;
-      if (xrow[i] != nullptr && k < K)
-        xr[i] = *reinterpret_cast<const uint4*>(xrow[i] + k);
-      else
-        xr[i] = make_uint4(0u, 0u, 0u, 0u);
-    }
-#pragma unroll
-    for (int i = 0; i < KT::kWChunks; ++i) {
-      const int k = k0 + wc[i] * KT::kWChunkElems;
-      if (wrow[i] != nullptr && k < K) {
-        const size_t boff = (FMT == kQ8) ? (size_t)k : (size_t)(k >> 1);
-        wr[i] = *reinterpret_cast<const uint4*>(wrow[i] + boff);
-        sr[i] = fp16_to_f32(srow[i][k >> 5]);
-      } else {
-        wr[i] = make_uint4(0u, 0u, 0u, 0u);
-        sr[i] = 0.0f;
-      }
+    for (int j = 0; j < KT::kXLoads; ++j) {
+      uint32_t off = (xoff[j] == kOOB) ? kOOB : xoff[j] + kbyte;
+      if (tail && (kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
+      lds_char* dst = lds + stage * KT::kStageBytes + (wave * KT::kXLoads + j) * 1024;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
     }
   };
 
-  auto store_step = [&](int buf) {
-    char* xs = lds + buf * KT::kTileBytes;
-    char* ws = xs + BM * kRowBytes;
-#pragma unroll
-    for (int i = 0; i < KT::kXChunks; ++i) {
-      const int q = tid + i * KT::kThreads;
-      *reinterpret_cast<uint4*>(xs + lds_chunk(q >> 3, q & 7)) = xr[i];
-    }
+  uint4 wv[2][KT::kWChunks];
+  uint32_t sv[2][KT::kWChunks];
+
+  auto issue_w = [&](int kt, uint4 (&w)[KT::kWChunks], uint32_t (&s)[KT::kWChunks]) {
 #pragma unroll
     for (int i = 0; i < KT::kWChunks; ++i) {
-      const int q = tid + i * KT::kThreads;
-      const int r = q / KT::kWChunksPerRow;
-      if constexpr (FMT == kQ8) {
-        uint32_t o[8];
-        dequant_q8x16(wr[i], sr[i], o);
-        const int c = wc[i] * 2;
-        *reinterpret_cast<uint4*>(ws + lds_chunk(r, c)) = make_uint4(o[0], o[1], o[2], o[3]);
-        *reinterpret_cast<uint4*>(ws + lds_chunk(r, c + 1)) = make_uint4(o[4], o[5], o[6], o[7]);
-      } else {
-        uint32_t o[16];
-        dequant_q4x32(wr[i], sr[i], o);
-        const int c = wc[i] * 4;
-#pragma unroll
-        for (int h = 0; h < 4; ++h)
-          *reinterpret_cast<uint4*>(ws + lds_chunk(r, c + h)) =
-              make_uint4(o[4 * h], o[4 * h + 1], o[4 * h + 2], o[4 * h + 3]);
+      w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                           wr, woff[i] + (uint32_t)kt * KT::kWStepBytes, 0, 0));
+      s[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(sr, soff[i] + (uint32_t)kt * 4u, 0, 0);
+    }
+  };
+
+  // dequantise unit u (0 <= u < kUnits) of a weight register set into LDS stage `stage`
+  float scl[KT::kWChunks], scl16[KT::kWChunks], soffv[KT::kWChunks];
+  auto dequant_unit = [&](int kt, int u, const uint4 (&w)[KT::kWChunks], const uint32_t (&s)[KT::kWChunks],
+                          int stage) {
+    const int i = u / kUnitsPerChunk;
+    const int sub = u % kUnitsPerChunk;
+    if (sub == 0) {
+      const bool valid = kt * kBK + wcol[i] * KT::kWChunkElems < K;
+      scl[i] = valid ? fp16_to_f32((uint16_t)s[i]) : 0.0f;
+      if constexpr (FMT == kQ4) {
+        scl16[i] = scl[i] * 0.0625f;
+        soffv[i] = -8.0f * scl[i];
       }
     }
+    const uint32_t d[4] = {w[i].x, w[i].y, w[i].z, w[i].w};
+    u32x4 o;
+    if constexpr (FMT == kQ8)
+      o = dequant_q8_unit(d[2 * sub], d[2 * sub + 1], scl[i]);
+    else
+      o = dequant_q4_unit(d[sub], scl[i], scl16[i], soffv[i]);
+    *reinterpret_cast<lds_u32x4*>(lds + stage * KT::kStageBytes + KT::kXTileBytes + lds_w[i][sub]) = o;
   };
 
   f32x16 acc[KT::kTM][KT::kTN];
@@ -238,57 +323,106 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  // 32-row MFMA blocks of this wave that hold at least one valid row
   const int wrow0 = wm * KT::kWTM;
-  const int mblocks = rows_valid <= wrow0 ? 0 : (rows_valid - wrow0 + 31) >> 5;
-
-  load_step(0);
-  store_step(0);
-  __syncthreads();
-
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = (kt + 1) < nk;
-    if (more) load_step(kt + 1);
-
-    const char* xs = lds + cur * KT::kTileBytes;
-    const char* ws = xs + BM * kRowBytes;
-    const int lr = lane & 31;
-    const int lh = lane >> 5;
+  const int mblocks = FULL ? KT::kTM : (rows_valid <= wrow0 ? 0 : (rows_valid - wrow0 + 31) >> 5);
+  const int lr = lane & 31;
+  const int lh = lane >> 5;
+  // per-lane LDS byte offsets of the A / B fragments of sub-step 0 (chunk lh); chunk 2 kk + lh
+  // of row r sits at r * 128 + (((2 kk + lh) ^ ((r >> 1) & 7)) << 4)
+  int aoff[KT::kTM], boff[KT::kTN];
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-      const int c = kk * 2 + lh;
-      bf16x8 bv[KT::kTN];
+  for (int i = 0; i < KT::kTM; ++i) aoff[i] = (wrow0 + i * 32 + lr) * kRowBytes;
+#pragma unroll
+  for (int j = 0; j < KT::kTN; ++j) boff[j] = (wn * KT::kWTN + j * 32 + lr) * kRowBytes;
+  const int rsw = ((lr >> 1) & 7);   // (r >> 1) & 7 is the same for every fragment row: bases are multiples of 32
+
+  // one K step over stage `cur`, dequantising step kt+1's weights (set wn_) into stage cur ^ 1
+  auto step = [&](int kt, int cur, const uint4 (&wn_)[KT::kWChunks], const uint32_t (&sn_)[KT::kWChunks]) {
+    const lds_char* xs = lds + cur * KT::kStageBytes;
+    const lds_char* ws = xs + KT::kXTileBytes;
+    const bool more = kt + 1 < nk;
+    bf16x8 av[2][KT::kTM], bv[2][KT::kTN];
+    auto load_frags = [&](int kk, int buf) {
+      const int slot = ((kk * 2 + lh) ^ rsw) << 4;
 #pragma unroll
       for (int j = 0; j < KT::kTN; ++j)
-        bv[j] = *reinterpret_cast<const bf16x8*>(ws + lds_chunk(wn * KT::kWTN + j * 32 + lr, c));
+        bv[buf][j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(ws + boff[j] + slot);
+#pragma unroll
+      for (int i = 0; i < KT::kTM; ++i)
+        av[buf][i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(xs + aoff[i] + slot);
+    };
+    load_frags(0, 0);
+    if constexpr (FULL) __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      const int buf = kk & 1;
+      if (kk + 1 < kBK / 16) load_frags(kk + 1, buf ^ 1);
 #pragma unroll
       for (int i = 0; i < KT::kTM; ++i) {
-        if (i < mblocks) {
-          const bf16x8 av = *reinterpret_cast<const bf16x8*>(xs + lds_chunk(wrow0 + i * 32 + lr, c));
+        if (FULL || i < mblocks) {
 #pragma unroll
           for (int j = 0; j < KT::kTN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[buf][i], bv[buf][j], acc[i][j], 0, 0, 0);
         }
       }
+      if (more) {
+#pragma unroll
+        for (int u = kk * kUnitsPerKK; u < (kk + 1) * kUnitsPerKK; ++u) dequant_unit(kt + 1, u, wn_, sn_, cur ^ 1);
+      }
+      if constexpr (FULL) {
+        // MFMA, next fragments' LDS reads, then VALU between the remaining MFMAs, LDS writes last
+        QG_SG(kSchedMFMA, 1);
+        if (kk + 1 < kBK / 16) QG_SG(kSchedDSRead, KT::kTM + KT::kTN);
+#pragma unroll
+        for (int m = 1; m < kMfmaPerKK; ++m) {
+          QG_SG(kSchedVALU, kValuPerMfma);
+          QG_SG(kSchedMFMA, 1);
+        }
+        QG_SG(kSchedVALU, kValuPerMfma);
+        QG_SG(kSchedDSWrite, kUnitsPerKK);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
+  };
 
-    if (more) store_step(cur ^ 1);
-    __syncthreads();
+  // prologue: step 0 staged, step 1 weights in flight
+  issue_x(0, 0);
+  issue_w(0, wv[0], sv[0]);
+  if (nk > 1) issue_w(1, wv[1], sv[1]);
+#pragma unroll
+  for (int u = 0; u < kUnits; ++u) dequant_unit(0, u, wv[0], sv[0], 0);
+  if (nk > 1) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
+  __builtin_amdgcn_s_barrier();
+
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    // even step: stage 0; weights of step kt+1 are in set 1; prefetch step kt+2 into set 0
+    issue_x(kt + 1, 1);
+    if (kt + 2 < nk) issue_w(kt + 2, wv[0], sv[0]);
+    step(kt, 0, wv[1], sv[1]);
+    if (kt + 2 < nk) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
+    // odd step: stage 1; weights of step kt+2 are in set 0; prefetch step kt+3 into set 1
+    if (kt + 2 < nk) issue_x(kt + 2, 0);
+    if (kt + 3 < nk) issue_w(kt + 3, wv[1], sv[1]);
+    step(kt + 1, 1, wv[0], sv[0]);
+    if (kt + 3 < nk) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
+  }
+  if (kt < nk) {   // odd number of steps: the last one runs on stage 0 with nothing left to fetch
+    step(kt, 0, wv[1], sv[1]);
   }
 
   // --- epilogue: lane holds column (lane & 31) and rows (r/4)*8 + (lane/32)*4 + r%4 of each block ---
-  const int lr = lane & 31;
-  const int lh = lane >> 5;
 #pragma unroll
   for (int i = 0; i < KT::kTM; ++i) {
     if (i >= mblocks) continue;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = wrow0 + i * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
-      if (row >= rows_valid) continue;
+      if (!FULL && row >= rows_valid) continue;
       const int dst = MOE ? s_yrow[row] : (m0 + row);
-      if (dst < 0) continue;
+      if (MOE && dst < 0) continue;
       float* yrow = a.y + (size_t)dst * N;
 #pragma unroll
       for (int j = 0; j < KT::kTN; ++j) {
@@ -299,11 +433,22 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   }
 }
 
+template <int FMT, int BM, int BN, int WM, int WN, bool MOE>
+__device__ __forceinline__ void tile_dispatch(const TileArgs& a, const uint8_t* __restrict__ wq,
+                                              const uint16_t* __restrict__ sc, int m0, int n0, int rows_valid,
+                                              const int* __restrict__ s_xrow, const int* __restrict__ s_yrow,
+                                              char* __restrict__ lds) {
+  if (rows_valid == BM)
+    tile_body<FMT, BM, BN, WM, WN, MOE, true>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds);
+  else
+    tile_body<FMT, BM, BN, WM, WN, MOE, false>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds);
+}
+
 template <int FMT, int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const uint8_t* __restrict__ wq,
                                                              const uint16_t* __restrict__ sc) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, false>;
-  __shared__ __attribute__((aligned(16))) char lds[KT::kLdsBytes];
+  __shared__ __attribute__((aligned(1024))) char lds[KT::kLdsBytes];
   const int mt_n = (a.M + BM - 1) / BM;
   const int nt_n = (a.N + BN - 1) / BN;
   const int ntiles = mt_n * nt_n;
@@ -313,7 +458,7 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
   const int mt = tile - nt * mt_n;
   const int m0 = mt * BM;
   const int rows_valid = min(BM, a.M - m0);
-  tile_body<FMT, BM, BN, WM, WN, false>(a, wq, sc, m0, nt * BN, rows_valid, nullptr, nullptr, lds);
+  tile_dispatch<FMT, BM, BN, WM, WN, false>(a, wq, sc, m0, nt * BN, rows_valid, nullptr, nullptr, lds);
 }
 
 // Grouped MoE GEMM: the launch covers experts [e_begin, e_begin + n_experts).
@@ -323,7 +468,8 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
 template <int FMT, int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtrs ep) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, true>;
-  __shared__ __attribute__((aligned(16))) char lds[KT::kLdsBytes];
+  static_assert(KT::kThreads >= kMaxExpertsPerLaunch, "the tile prefix needs one lane per expert");
+  __shared__ __attribute__((aligned(1024))) char lds[KT::kLdsBytes];
   __shared__ int s_prefix[kMaxExpertsPerLaunch + 1];
   __shared__ int s_rowidx[BM];   // y row (assignment) of each tile row
   __shared__ int s_xrow[BM];     // x row (token = assignment / topk) of each tile row
@@ -331,19 +477,31 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtr
   const int nt_n = (a.N + BN - 1) / BN;
   const int ne = a.n_experts;
 
-  // per-expert tile counts -> inclusive prefix (one thread; at most 128 experts)
-  if (tid == 0) {
-    int run = 0;
-    s_prefix[0] = 0;
-    for (int e = 0; e < ne; ++e) {
-      const int lo = a.offsets[a.e_begin + e];
-      const int hi = a.offsets[a.e_begin + e + 1];
+  // per-expert tile counts -> inclusive prefix over the launch's experts (<= 128):
+  // one expert per lane of the first two waves, wave prefix sums, then combine.
+  __shared__ int s_wsum[2];
+  if (tid < 128) {
+    int tiles = 0;
+    if (tid < ne) {
+      const int lo = a.offsets[a.e_begin + tid];
+      const int hi = a.offsets[a.e_begin + tid + 1];
       int c = hi - lo;
       if (lo < 0 || hi > a.M || c < 0) c = 0;   // inconsistent table: no work for this expert
-      run += ((c + BM - 1) / BM) * nt_n;
-      s_prefix[e + 1] = run;
+      const long t = ((long)c + BM - 1) / BM * nt_n;
+      tiles = (int)(t < (1L << 23) ? t : (1L << 23));   // keeps the sum of 128 experts below 2^31
     }
+    int incl = tiles;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int v = __shfl_up(incl, d, 64);
+      if ((tid & 63) >= d) incl += v;
+    }
+    if ((tid & 63) == 63) s_wsum[tid >> 6] = incl;
+    s_prefix[tid + 1] = incl;
+    if (tid == 0) s_prefix[0] = 0;
   }
+  __syncthreads();
+  if (tid >= 64 && tid < 128) s_prefix[tid + 1] += s_wsum[0];
   __syncthreads();
   const int ntiles = s_prefix[ne];
   if ((int)blockIdx.x >= ntiles) return;
@@ -371,7 +529,7 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtr
     s_xrow[r] = asg < 0 ? -1 : asg / a.topk;
   }
   __syncthreads();
-  tile_body<FMT, BM, BN, WM, WN, true>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow, s_rowidx, lds);
+  tile_dispatch<FMT, BM, BN, WM, WN, true>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow, s_rowidx, lds);
 }
 
 }  // namespace qg
