@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seconds", type=float, default=15.0)
+    ap.add_argument("--no-events", action="store_true",
+                    help="time the step without per-launch events (then no roofline figure)")
     ap.add_argument("--only", default="", help="comma list of parts to run: dense_gate_up,dense_down,moe_t2048,moe_t8192")
     return ap.parse_args()
 
@@ -225,7 +227,7 @@ def main():
     log("warmup done")
 
     # timed region: whole-job wall time, with per-launch events on the launching stream
-    timer = EventTimer(torch, True)
+    timer = EventTimer(torch, not args.no_events)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -239,6 +241,9 @@ def main():
     flops_step = sum(p.flops for p in parts)
     value = flops_step / (wall / args.steps) / 1e12
 
+    if args.no_events:
+        print(json.dumps({"ms_per_step": ms_per_step, "value": value}), flush=True)
+        return 0
     per = timer.summary()
     flops_of = {}
     for p in parts:

@@ -64,7 +64,7 @@ int launch_dense(const qg::TileArgs& a, const void* wq, const void* sc, hipStrea
 template <int FMT>
 int dense_dispatch(const qg::TileArgs& a, const void* wq, const void* sc, hipStream_t s) {
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
-  if (a.M >= 256 && a.N >= 256 && big >= 200) return launch_dense<FMT, 256, 256, 2, 2>(a, wq, sc, s);
+  if (a.M >= 256 && a.N >= 256 && big >= 200) return launch_dense<FMT, 256, 256, 2, 4>(a, wq, sc, s);
   return launch_dense<FMT, 128, 128, 2, 2>(a, wq, sc, s);
 }
 

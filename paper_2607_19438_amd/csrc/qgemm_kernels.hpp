@@ -336,53 +336,67 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   for (int j = 0; j < KT::kTN; ++j) boff[j] = (wn * KT::kWTN + j * 32 + lr) * kRowBytes;
   const int rsw = ((lr >> 1) & 7);   // (r >> 1) & 7 is the same for every fragment row: bases are multiples of 32
 
-  // one K step over stage `cur`, dequantising step kt+1's weights (set wn_) into stage cur ^ 1
-  auto step = [&](int kt, int cur, const uint4 (&wn_)[KT::kWChunks], const uint32_t (&sn_)[KT::kWChunks]) {
-    const lds_char* xs = lds + cur * KT::kStageBytes;
+  // Fragment registers: sub-step kk uses set kk & 1. The last sub-step's MFMAs run after
+  // the barrier that closes the K step, overlapping the next step's first LDS reads.
+  bf16x8 av[2][KT::kTM], bv[2][KT::kTN];
+  auto load_frags = [&](int stage, int kk, int buf) {
+    const lds_char* xs = lds + stage * KT::kStageBytes;
     const lds_char* ws = xs + KT::kXTileBytes;
-    const bool more = kt + 1 < nk;
-    bf16x8 av[2][KT::kTM], bv[2][KT::kTN];
-    auto load_frags = [&](int kk, int buf) {
-      const int slot = ((kk * 2 + lh) ^ rsw) << 4;
+    const int slot = ((kk * 2 + lh) ^ rsw) << 4;
 #pragma unroll
-      for (int j = 0; j < KT::kTN; ++j)
-        bv[buf][j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(ws + boff[j] + slot);
+    for (int j = 0; j < KT::kTN; ++j)
+      bv[buf][j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(ws + boff[j] + slot);
 #pragma unroll
-      for (int i = 0; i < KT::kTM; ++i)
-        av[buf][i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(xs + aoff[i] + slot);
-    };
-    load_frags(0, 0);
-    if constexpr (FULL) __builtin_amdgcn_sched_barrier(0);
+    for (int i = 0; i < KT::kTM; ++i)
+      av[buf][i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(xs + aoff[i] + slot);
+  };
+  auto mfmas = [&](int buf) {
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
+    for (int i = 0; i < KT::kTM; ++i) {
+      if (FULL || i < mblocks) {
+#pragma unroll
+        for (int j = 0; j < KT::kTN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[buf][i], bv[buf][j], acc[i][j], 0, 0, 0);
+      }
+    }
+  };
+  // dequantisation units of the next step, spread over sub-steps 0..2 (they must land before the barrier)
+  constexpr int kUnitGroups = 3;
+  auto unit_lo = [](int kk) { return (kk * kUnits + kUnitGroups - 1) / kUnitGroups; };
+
+  // sub-steps 0..2 of step kt over stage `cur` (fragments of sub-step 0 already in set 0), with
+  // step kt+1's weights (set wn_) dequantised into stage cur ^ 1; leaves sub-step 3's fragments in set 1
+  auto step_head = [&](int kt, int cur, const uint4 (&wn_)[KT::kWChunks], const uint32_t (&sn_)[KT::kWChunks]) {
+#pragma unroll
+    for (int kk = 0; kk < 3; ++kk) {
       const int buf = kk & 1;
-      if (kk + 1 < kBK / 16) load_frags(kk + 1, buf ^ 1);
+      load_frags(cur, kk + 1, buf ^ 1);
+      mfmas(buf);
+      // step kt+1's weights (on the last step this writes the idle stage with unused data:
+      // harmless, and it keeps the body branch-free for the MFMA/VALU interleave)
 #pragma unroll
-      for (int i = 0; i < KT::kTM; ++i) {
-        if (FULL || i < mblocks) {
-#pragma unroll
-          for (int j = 0; j < KT::kTN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[buf][i], bv[buf][j], acc[i][j], 0, 0, 0);
-        }
-      }
-      if (more) {
-#pragma unroll
-        for (int u = kk * kUnitsPerKK; u < (kk + 1) * kUnitsPerKK; ++u) dequant_unit(kt + 1, u, wn_, sn_, cur ^ 1);
-      }
+      for (int u = unit_lo(kk); u < unit_lo(kk + 1); ++u) dequant_unit(kt + 1, u, wn_, sn_, cur ^ 1);
       if constexpr (FULL) {
-        // MFMA, next fragments' LDS reads, then VALU between the remaining MFMAs, LDS writes last
+        constexpr int kUnitsHere = kUnits / kUnitGroups + 1;
+        constexpr int kVpm = (kUnitsHere * kValuPerUnit + 4 + kMfmaPerKK - 1) / kMfmaPerKK;
         QG_SG(kSchedMFMA, 1);
-        if (kk + 1 < kBK / 16) QG_SG(kSchedDSRead, KT::kTM + KT::kTN);
+        QG_SG(kSchedDSRead, KT::kTM + KT::kTN);
 #pragma unroll
         for (int m = 1; m < kMfmaPerKK; ++m) {
-          QG_SG(kSchedVALU, kValuPerMfma);
+          QG_SG(kSchedVALU, kVpm);
           QG_SG(kSchedMFMA, 1);
         }
-        QG_SG(kSchedVALU, kValuPerMfma);
-        QG_SG(kSchedDSWrite, kUnitsPerKK);
+        QG_SG(kSchedVALU, kVpm);
+        QG_SG(kSchedDSWrite, kUnitsHere);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+  };
+  // after the barrier: next step's sub-step 0 fragments (if any) while sub-step 3's MFMAs run
+  auto step_tail = [&](bool next, int next_stage) {
+    if (next) load_frags(next_stage, 0, 0);
+    mfmas(1);
+    if constexpr (FULL) __builtin_amdgcn_sched_barrier(0);
   };
 
   // prologue: step 0 staged, step 1 weights in flight
@@ -393,41 +407,50 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   for (int u = 0; u < kUnits; ++u) dequant_unit(0, u, wv[0], sv[0], 0);
   if (nk > 1) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
   __builtin_amdgcn_s_barrier();
+  load_frags(0, 0, 0);
 
   int kt = 0;
   for (; kt + 1 < nk; kt += 2) {
     // even step: stage 0; weights of step kt+1 are in set 1; prefetch step kt+2 into set 0
     issue_x(kt + 1, 1);
     if (kt + 2 < nk) issue_w(kt + 2, wv[0], sv[0]);
-    step(kt, 0, wv[1], sv[1]);
+    step_head(kt, 0, wv[1], sv[1]);
     if (kt + 2 < nk) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
     __builtin_amdgcn_s_barrier();
+    step_tail(true, 1);
     // odd step: stage 1; weights of step kt+2 are in set 0; prefetch step kt+3 into set 1
     if (kt + 2 < nk) issue_x(kt + 2, 0);
     if (kt + 3 < nk) issue_w(kt + 3, wv[1], sv[1]);
-    step(kt + 1, 1, wv[0], sv[0]);
+    step_head(kt + 1, 1, wv[0], sv[0]);
     if (kt + 3 < nk) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
     __builtin_amdgcn_s_barrier();
+    step_tail(kt + 2 < nk, 0);
   }
   if (kt < nk) {   // odd number of steps: the last one runs on stage 0 with nothing left to fetch
-    step(kt, 0, wv[1], sv[1]);
+    step_head(kt, 0, wv[1], sv[1]);
+    wait_vmcnt_lgkm0<0>();
+    step_tail(false, 0);
   }
 
   // --- epilogue: lane holds column (lane & 31) and rows (r/4)*8 + (lane/32)*4 + r%4 of each block ---
+  const bool full_cols = n0 + BN <= N;
 #pragma unroll
   for (int i = 0; i < KT::kTM; ++i) {
-    if (i >= mblocks) continue;
+    if (!FULL && i >= mblocks) continue;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = wrow0 + i * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
       if (!FULL && row >= rows_valid) continue;
       const int dst = MOE ? s_yrow[row] : (m0 + row);
       if (MOE && dst < 0) continue;
-      float* yrow = a.y + (size_t)dst * N;
+      float* yrow = a.y + (size_t)dst * N + n0 + wn * KT::kWTN + lr;
+      if (full_cols) {
 #pragma unroll
-      for (int j = 0; j < KT::kTN; ++j) {
-        const int col = n0 + wn * KT::kWTN + j * 32 + lr;
-        if (col < N) yrow[col] = acc[i][j][r];
+        for (int j = 0; j < KT::kTN; ++j) yrow[j * 32] = acc[i][j][r];
+      } else {
+#pragma unroll
+        for (int j = 0; j < KT::kTN; ++j)
+          if (n0 + wn * KT::kWTN + j * 32 + lr < N) yrow[j * 32] = acc[i][j][r];
       }
     }
   }
