@@ -52,11 +52,11 @@ int check_common(int N, int K, int fmt) {
 // kernel selection
 // ---------------------------------------------------------------------------
 
-template <int FMT, int BM, int BN, int WM, int WN>
+template <int FMT, int BM, int BN, int WM, int WN, int XS>
 int launch_dense(const qg::TileArgs& a, const void* wq, const void* sc, hipStream_t s) {
   const long tiles = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   if (tiles > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "too many tiles");
-  hipLaunchKernelGGL((qg::dense_kernel<FMT, BM, BN, WM, WN>), dim3((unsigned)tiles), dim3(WM * WN * 64), 0, s, a,
+  hipLaunchKernelGGL((qg::dense_kernel<FMT, BM, BN, WM, WN, XS>), dim3((unsigned)tiles), dim3(WM * WN * 64), 0, s, a,
                      static_cast<const uint8_t*>(wq), static_cast<const uint16_t*>(sc));
   return check_launch("qgemm_dense");
 }
@@ -64,16 +64,13 @@ int launch_dense(const qg::TileArgs& a, const void* wq, const void* sc, hipStrea
 template <int FMT>
 int dense_dispatch(const qg::TileArgs& a, const void* wq, const void* sc, hipStream_t s) {
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
-  if (a.M >= 256 && a.N >= 256 && big >= 200) return launch_dense<FMT, 256, 256, 2, 4>(a, wq, sc, s);
-  return launch_dense<FMT, 128, 128, 2, 2>(a, wq, sc, s);
+  if (a.M >= 256 && a.N >= 256 && big >= 200) return launch_dense<FMT, 256, 256, 2, 4, 2>(a, wq, sc, s);
+  return launch_dense<FMT, 128, 128, 2, 2, 2>(a, wq, sc, s);
 }
 
-constexpr int kMoeBM = 128;
-constexpr int kMoeBN = 128;
-
-template <int FMT>
-int launch_moe(qg::TileArgs a, const void* const* wq, const void* const* sc, int E, hipStream_t s) {
-  const int nt = (a.N + kMoeBN - 1) / kMoeBN;
+template <int FMT, int BM, int BN, int WM, int WN, int XS>
+int launch_moe_cfg(qg::TileArgs a, const void* const* wq, const void* const* sc, int E, hipStream_t s) {
+  const int nt = (a.N + BN - 1) / BN;
   for (int e0 = 0; e0 < E; e0 += qg::kMaxExpertsPerLaunch) {
     const int ne = (E - e0) < qg::kMaxExpertsPerLaunch ? (E - e0) : qg::kMaxExpertsPerLaunch;
     qg::ExpertPtrs ep;
@@ -83,15 +80,25 @@ int launch_moe(qg::TileArgs a, const void* const* wq, const void* const* sc, int
     }
     a.e_begin = e0;
     a.n_experts = ne;
-    // upper bound of sum_e ceil(c_e / BM) over the launch's experts
-    const long mt_bound = (long)(a.M + kMoeBM - 1) / kMoeBM + ne;
+    // upper bound of sum_e ceil(c_e / BM) over the launch's experts; workgroups past the
+    // real tile count exit at once
+    const long mt_bound = (long)(a.M + BM - 1) / BM + ne;
     const long grid = mt_bound * nt;
     if (grid > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "too many tiles");
-    hipLaunchKernelGGL((qg::moe_kernel<FMT, kMoeBM, kMoeBN, 2, 2>), dim3((unsigned)grid), dim3(256), 0, s, a, ep);
+    hipLaunchKernelGGL((qg::moe_kernel<FMT, BM, BN, WM, WN, XS>), dim3((unsigned)grid), dim3(WM * WN * 64), 0, s, a, ep);
     const int rc = check_launch("qgemm_moe");
     if (rc != QGEMM_OK) return rc;
   }
   return QGEMM_OK;
+}
+
+// Tile height from the mean rows per expert (the host does not see the routing): groups of
+// about 100-200 rows fit one 192-row tile each; larger groups use 256-row tiles.
+template <int FMT>
+int launch_moe(qg::TileArgs a, const void* const* wq, const void* const* sc, int E, hipStream_t s) {
+  const long mean_rows = (long)a.M / E;
+  if (mean_rows > 192) return launch_moe_cfg<FMT, 256, 256, 2, 4, 2>(a, wq, sc, E, s);
+  return launch_moe_cfg<FMT, 192, 256, 2, 4, 2>(a, wq, sc, E, s);
 }
 
 // ---------------------------------------------------------------------------

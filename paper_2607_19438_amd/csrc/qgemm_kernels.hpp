@@ -150,7 +150,7 @@ __device__ __forceinline__ int xcd_tile(int bid, int ntiles) {
   return xcd * base + (xcd < rem ? xcd : rem) + local;
 }
 
-template <int FMT, int BM, int BN, int WM, int WN, bool MOE>
+template <int FMT, int BM, int BN, int WM, int WN, bool MOE, int XS = 2>
 struct TileKernel {
   static constexpr int kThreads = WM * WN * 64;
   static constexpr int kWaves = WM * WN;
@@ -164,8 +164,11 @@ struct TileKernel {
   static constexpr int kWStepBytes = (FMT == kQ8) ? kBK : kBK / 2;   // packed bytes of one row per K step
   static constexpr int kWChunks = BN * kWChunksPerRow / kThreads;
   static constexpr int kXTileBytes = BM * kRowBytes;
-  static constexpr int kStageBytes = (BM + BN) * kRowBytes;
-  static constexpr int kLdsBytes = 2 * kStageBytes;
+  static constexpr int kWTileBytes = BN * kRowBytes;
+  static constexpr int kXStages = XS;                            // activation stages (DMA runs XS-1 steps ahead)
+  static constexpr int kWBase = XS * kXTileBytes;                 // weight stages follow the activation stages
+  static constexpr int kLdsBytes = XS * kXTileBytes + 2 * kWTileBytes;
+  static_assert(XS == 2 || XS == 3, "two or three activation stages");
   static_assert(kXLoads * kWaves * 8 == BM, "x tile must split into 8-row groups per wave");
   static_assert(kWChunks * kThreads == BN * kWChunksPerRow, "w tile must split evenly");
   static_assert(kTM >= 1 && kTN >= 1, "wave tile must hold a 32x32 block");
@@ -197,12 +200,12 @@ constexpr int kSchedDSWrite = 0x200;
 //   (kt+1)&1) interleaved between them
 //   wait for the activation DMA and the LDS writes, then barrier
 // FULL: every row of the tile is valid, so no MFMA is skipped (branch-free body).
-template <int FMT, int BM, int BN, int WM, int WN, bool MOE, bool FULL>
+template <int FMT, int BM, int BN, int WM, int WN, bool MOE, bool FULL, int XS>
 __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __restrict__ wq,
                                           const uint16_t* __restrict__ sc, int m0, int n0,
                                           int rows_valid, const int* __restrict__ s_xrow,
                                           const int* __restrict__ s_yrow, char* __restrict__ lds_generic) {
-  using KT = TileKernel<FMT, BM, BN, WM, WN, MOE>;
+  using KT = TileKernel<FMT, BM, BN, WM, WN, MOE, XS>;
   constexpr int kUnitsPerChunk = (FMT == kQ8) ? 2 : 4;        // 16-byte LDS writes per 16-byte load
   constexpr int kUnits = KT::kWChunks * kUnitsPerChunk;        // per thread per K step
   static_assert(kUnits % 4 == 0, "units must spread evenly over the four K16 sub-steps");
@@ -275,7 +278,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     for (int j = 0; j < KT::kXLoads; ++j) {
       uint32_t off = (xoff[j] == kOOB) ? kOOB : xoff[j] + kbyte;
       if (tail && (kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
-      lds_char* dst = lds + stage * KT::kStageBytes + (wave * KT::kXLoads + j) * 1024;
+      lds_char* dst = lds + stage * KT::kXTileBytes + (wave * KT::kXLoads + j) * 1024;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
     }
   };
@@ -312,7 +315,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       o = dequant_q8_unit(d[2 * sub], d[2 * sub + 1], scl[i]);
     else
       o = dequant_q4_unit(d[sub], scl[i], scl16[i], soffv[i]);
-    *reinterpret_cast<lds_u32x4*>(lds + stage * KT::kStageBytes + KT::kXTileBytes + lds_w[i][sub]) = o;
+    *reinterpret_cast<lds_u32x4*>(lds + KT::kWBase + stage * KT::kWTileBytes + lds_w[i][sub]) = o;
   };
 
   f32x16 acc[KT::kTM][KT::kTN];
@@ -323,15 +326,17 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int wrow0 = wm * KT::kWTM;
-  const int mblocks = FULL ? KT::kTM : (rows_valid <= wrow0 ? 0 : (rows_valid - wrow0 + 31) >> 5);
+  // 32-row block i of this wave is tile block i * WM + wm (blocks dealt round-robin over the
+  // WM wave rows, so a partly filled tile spreads its valid blocks evenly over the waves)
+  const int nvalid_blocks = (rows_valid + 31) >> 5;
+  const int mblocks = FULL ? KT::kTM : (nvalid_blocks > wm ? (nvalid_blocks - wm + WM - 1) / WM : 0);
   const int lr = lane & 31;
   const int lh = lane >> 5;
   // per-lane LDS byte offsets of the A / B fragments of sub-step 0 (chunk lh); chunk 2 kk + lh
   // of row r sits at r * 128 + (((2 kk + lh) ^ ((r >> 1) & 7)) << 4)
   int aoff[KT::kTM], boff[KT::kTN];
 #pragma unroll
-  for (int i = 0; i < KT::kTM; ++i) aoff[i] = (wrow0 + i * 32 + lr) * kRowBytes;
+  for (int i = 0; i < KT::kTM; ++i) aoff[i] = ((i * WM + wm) * 32 + lr) * kRowBytes;
 #pragma unroll
   for (int j = 0; j < KT::kTN; ++j) boff[j] = (wn * KT::kWTN + j * 32 + lr) * kRowBytes;
   const int rsw = ((lr >> 1) & 7);   // (r >> 1) & 7 is the same for every fragment row: bases are multiples of 32
@@ -339,9 +344,9 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   // Fragment registers: sub-step kk uses set kk & 1. The last sub-step's MFMAs run after
   // the barrier that closes the K step, overlapping the next step's first LDS reads.
   bf16x8 av[2][KT::kTM], bv[2][KT::kTN];
-  auto load_frags = [&](int stage, int kk, int buf) {
-    const lds_char* xs = lds + stage * KT::kStageBytes;
-    const lds_char* ws = xs + KT::kXTileBytes;
+  auto load_frags = [&](int xstage, int wstage, int kk, int buf) {
+    const lds_char* xs = lds + xstage * KT::kXTileBytes;
+    const lds_char* ws = lds + KT::kWBase + wstage * KT::kWTileBytes;
     const int slot = ((kk * 2 + lh) ^ rsw) << 4;
 #pragma unroll
     for (int j = 0; j < KT::kTN; ++j)
@@ -364,18 +369,20 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   constexpr int kUnitGroups = 3;
   auto unit_lo = [](int kk) { return (kk * kUnits + kUnitGroups - 1) / kUnitGroups; };
 
-  // sub-steps 0..2 of step kt over stage `cur` (fragments of sub-step 0 already in set 0), with
-  // step kt+1's weights (set wn_) dequantised into stage cur ^ 1; leaves sub-step 3's fragments in set 1
-  auto step_head = [&](int kt, int cur, const uint4 (&wn_)[KT::kWChunks], const uint32_t (&sn_)[KT::kWChunks]) {
+  // sub-steps 0..2 of step kt over activation stage xcur and weight stage wcur (fragments of
+  // sub-step 0 already in set 0), with step kt+1's weights (set wn_) dequantised into weight
+  // stage wcur ^ 1; leaves sub-step 3's fragments in set 1
+  auto step_head = [&](int kt, int xcur, int wcur, const uint4 (&wn_)[KT::kWChunks],
+                       const uint32_t (&sn_)[KT::kWChunks]) {
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk) {
       const int buf = kk & 1;
-      load_frags(cur, kk + 1, buf ^ 1);
+      load_frags(xcur, wcur, kk + 1, buf ^ 1);
       mfmas(buf);
       // step kt+1's weights (on the last step this writes the idle stage with unused data:
       // harmless, and it keeps the body branch-free for the MFMA/VALU interleave)
 #pragma unroll
-      for (int u = unit_lo(kk); u < unit_lo(kk + 1); ++u) dequant_unit(kt + 1, u, wn_, sn_, cur ^ 1);
+      for (int u = unit_lo(kk); u < unit_lo(kk + 1); ++u) dequant_unit(kt + 1, u, wn_, sn_, wcur ^ 1);
       if constexpr (FULL) {
         constexpr int kUnitsHere = kUnits / kUnitGroups + 1;
         constexpr int kVpm = (kUnitsHere * kValuPerUnit + 4 + kMfmaPerKK - 1) / kMfmaPerKK;
@@ -393,43 +400,69 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     }
   };
   // after the barrier: next step's sub-step 0 fragments (if any) while sub-step 3's MFMAs run
-  auto step_tail = [&](bool next, int next_stage) {
-    if (next) load_frags(next_stage, 0, 0);
+  auto step_tail = [&](bool next, int next_xstage, int next_wstage) {
+    if (next) load_frags(next_xstage, next_wstage, 0, 0);
     mfmas(1);
     if constexpr (FULL) __builtin_amdgcn_sched_barrier(0);
   };
 
-  // prologue: step 0 staged, step 1 weights in flight
+  // prologue: steps 0 .. XS-2 of the activations and steps 0, 1 of the weights in flight;
+  // step 0's weights dequantised into weight stage 0
+  constexpr int kAhead = XS - 1;                              // activation prefetch distance (steps)
+  constexpr int kPerStep = KT::kXLoads + 2 * KT::kWChunks;    // memory ops issued per K step
+  // vmcnt retires in issue order, so waiting for a weight register set also waits for every
+  // load issued before it: with three activation stages the weights of a step are issued
+  // before its activations, so dequantising them never forces the younger activations.
   issue_x(0, 0);
   issue_w(0, wv[0], sv[0]);
   if (nk > 1) issue_w(1, wv[1], sv[1]);
+  if (XS == 3 && nk > 1) issue_x(1, 1);
 #pragma unroll
   for (int u = 0; u < kUnits; ++u) dequant_unit(0, u, wv[0], sv[0], 0);
-  if (nk > 1) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
+  // step 0's activations landed: allow what was issued after them to stay in flight
+  if (nk > 1) {
+    if constexpr (XS == 3) wait_vmcnt_lgkm0<kPerStep>(); else wait_vmcnt_lgkm0<2 * KT::kWChunks>();
+  } else {
+    wait_vmcnt_lgkm0<0>();
+  }
   __builtin_amdgcn_s_barrier();
-  load_frags(0, 0, 0);
+  load_frags(0, 0, 0, 0);
 
+  // Step kt: issue activations of step kt+kAhead and weights of step kt+2, MFMA over
+  // activation stage kt % XS / weight stage kt & 1, then wait for step kt+1's activations.
+  // With two activation stages only one step of activations is in flight at the barrier
+  // (vmcnt counts the weight loads issued after it); with three, one more step's loads are.
+  auto xstage = [&](int k) { return XS == 2 ? (k & 1) : (k % 3); };
+  auto wait_next = [&](int k) {
+    if constexpr (XS == 3) {
+      if (k + 2 < nk) wait_vmcnt_lgkm0<kPerStep>(); else wait_vmcnt_lgkm0<0>();
+    } else {
+      if (k + 2 < nk) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
+    }
+  };
   int kt = 0;
   for (; kt + 1 < nk; kt += 2) {
-    // even step: stage 0; weights of step kt+1 are in set 1; prefetch step kt+2 into set 0
-    issue_x(kt + 1, 1);
+    // even step: weights of step kt+1 are in set 1; prefetch step kt+2's weights into set 0
+    if (XS == 2 && kt + kAhead < nk) issue_x(kt + kAhead, xstage(kt + kAhead));
     if (kt + 2 < nk) issue_w(kt + 2, wv[0], sv[0]);
-    step_head(kt, 0, wv[1], sv[1]);
-    if (kt + 2 < nk) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
+    if (XS == 3 && kt + kAhead < nk) issue_x(kt + kAhead, xstage(kt + kAhead));
+    step_head(kt, xstage(kt), 0, wv[1], sv[1]);
+    wait_next(kt);
     __builtin_amdgcn_s_barrier();
-    step_tail(true, 1);
-    // odd step: stage 1; weights of step kt+2 are in set 0; prefetch step kt+3 into set 1
-    if (kt + 2 < nk) issue_x(kt + 2, 0);
+    step_tail(true, xstage(kt + 1), 1);
+    // odd step: weights of step kt+2 are in set 0; prefetch step kt+3's weights into set 1
+    if (XS == 2 && kt + 1 + kAhead < nk) issue_x(kt + 1 + kAhead, xstage(kt + 1 + kAhead));
     if (kt + 3 < nk) issue_w(kt + 3, wv[1], sv[1]);
-    step_head(kt + 1, 1, wv[0], sv[0]);
-    if (kt + 3 < nk) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
+    if (XS == 3 && kt + 1 + kAhead < nk) issue_x(kt + 1 + kAhead, xstage(kt + 1 + kAhead));
+    step_head(kt + 1, xstage(kt + 1), 1, wv[0], sv[0]);
+    wait_next(kt + 1);
     __builtin_amdgcn_s_barrier();
-    step_tail(kt + 2 < nk, 0);
+    step_tail(kt + 2 < nk, xstage(kt + 2), 0);
   }
-  if (kt < nk) {   // odd number of steps: the last one runs on stage 0 with nothing left to fetch
-    step_head(kt, 0, wv[1], sv[1]);
+  if (kt < nk) {   // odd number of steps: the last one (weight stage 0) has nothing left to fetch
+    step_head(kt, xstage(kt), 0, wv[1], sv[1]);
     wait_vmcnt_lgkm0<0>();
-    step_tail(false, 0);
+    step_tail(false, 0, 0);
   }
 
   // --- epilogue: lane holds column (lane & 31) and rows (r/4)*8 + (lane/32)*4 + r%4 of each block ---
@@ -439,7 +472,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     if (!FULL && i >= mblocks) continue;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = wrow0 + i * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+      const int row = (i * WM + wm) * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
       if (!FULL && row >= rows_valid) continue;
       const int dst = MOE ? s_yrow[row] : (m0 + row);
       if (MOE && dst < 0) continue;
@@ -456,21 +489,21 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   }
 }
 
-template <int FMT, int BM, int BN, int WM, int WN, bool MOE>
+template <int FMT, int BM, int BN, int WM, int WN, bool MOE, int XS>
 __device__ __forceinline__ void tile_dispatch(const TileArgs& a, const uint8_t* __restrict__ wq,
                                               const uint16_t* __restrict__ sc, int m0, int n0, int rows_valid,
                                               const int* __restrict__ s_xrow, const int* __restrict__ s_yrow,
                                               char* __restrict__ lds) {
   if (rows_valid == BM)
-    tile_body<FMT, BM, BN, WM, WN, MOE, true>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds);
+    tile_body<FMT, BM, BN, WM, WN, MOE, true, XS>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds);
   else
-    tile_body<FMT, BM, BN, WM, WN, MOE, false>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds);
+    tile_body<FMT, BM, BN, WM, WN, MOE, false, XS>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds);
 }
 
-template <int FMT, int BM, int BN, int WM, int WN>
+template <int FMT, int BM, int BN, int WM, int WN, int XS>
 __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const uint8_t* __restrict__ wq,
                                                              const uint16_t* __restrict__ sc) {
-  using KT = TileKernel<FMT, BM, BN, WM, WN, false>;
+  using KT = TileKernel<FMT, BM, BN, WM, WN, false, XS>;
   __shared__ __attribute__((aligned(1024))) char lds[KT::kLdsBytes];
   const int mt_n = (a.M + BM - 1) / BM;
   const int nt_n = (a.N + BN - 1) / BN;
@@ -481,16 +514,16 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
   const int mt = tile - nt * mt_n;
   const int m0 = mt * BM;
   const int rows_valid = min(BM, a.M - m0);
-  tile_dispatch<FMT, BM, BN, WM, WN, false>(a, wq, sc, m0, nt * BN, rows_valid, nullptr, nullptr, lds);
+  tile_dispatch<FMT, BM, BN, WM, WN, false, XS>(a, wq, sc, m0, nt * BN, rows_valid, nullptr, nullptr, lds);
 }
 
 // Grouped MoE GEMM: the launch covers experts [e_begin, e_begin + n_experts).
 // Work items are (expert, m tile, n tile) over active experts only; every
 // workgroup decodes its item from the per-expert counts, so the host never
 // needs the routing.
-template <int FMT, int BM, int BN, int WM, int WN>
+template <int FMT, int BM, int BN, int WM, int WN, int XS>
 __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtrs ep) {
-  using KT = TileKernel<FMT, BM, BN, WM, WN, true>;
+  using KT = TileKernel<FMT, BM, BN, WM, WN, true, XS>;
   static_assert(KT::kThreads >= kMaxExpertsPerLaunch, "the tile prefix needs one lane per expert");
   __shared__ __attribute__((aligned(1024))) char lds[KT::kLdsBytes];
   __shared__ int s_prefix[kMaxExpertsPerLaunch + 1];
@@ -552,7 +585,7 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtr
     s_xrow[r] = asg < 0 ? -1 : asg / a.topk;
   }
   __syncthreads();
-  tile_dispatch<FMT, BM, BN, WM, WN, true>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow, s_rowidx, lds);
+  tile_dispatch<FMT, BM, BN, WM, WN, true, XS>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow, s_rowidx, lds);
 }
 
 }  // namespace qg
