@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -54,17 +55,67 @@ int check_common(int N, int K, int fmt) {
 
 template <int FMT, int BM, int BN, int WM, int WN, int XS>
 int launch_dense(const qg::TileArgs& a, const void* wq, const void* sc, hipStream_t s) {
-  const long tiles = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  const long tiles = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * a.splits;
   if (tiles > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "too many tiles");
   hipLaunchKernelGGL((qg::dense_kernel<FMT, BM, BN, WM, WN, XS>), dim3((unsigned)tiles), dim3(WM * WN * 64), 0, s, a,
                      static_cast<const uint8_t*>(wq), static_cast<const uint16_t*>(sc));
   return check_launch("qgemm_dense");
 }
 
+// split-K partials (per device; grown on first use, then reused)
+std::mutex g_split_mutex;
+std::vector<std::pair<float*, size_t>> g_split_ws;
+
+int split_workspace(size_t floats, float** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(QGEMM_EHIP, "hipGetDevice failed");
+  }
+  if ((int)g_split_ws.size() <= dev) g_split_ws.resize(dev + 1, {nullptr, 0});
+  auto& w = g_split_ws[dev];
+  if (w.second < floats) {
+    if (w.first) (void)hipFree(w.first);   // waits for work that may still use it
+    w = {nullptr, 0};
+    if (hipMalloc(reinterpret_cast<void**>(&w.first), floats * sizeof(float)) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(QGEMM_EHIP, "hipMalloc of %zu bytes for split-K partials failed", floats * sizeof(float));
+    }
+    w.second = floats;
+  }
+  *out = w.first;
+  return QGEMM_OK;
+}
+
+constexpr int kMinStepsPerSplit = 12;
+
 template <int FMT>
-int dense_dispatch(const qg::TileArgs& a, const void* wq, const void* sc, hipStream_t s) {
+int dense_dispatch(qg::TileArgs a, const void* wq, const void* sc, hipStream_t s) {
+  a.splits = 1;
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
   if (a.M >= 256 && a.N >= 256 && big >= 200) return launch_dense<FMT, 256, 256, 2, 4, 2>(a, wq, sc, s);
+  // few 256x256 tiles but a long K: split K over several workgroups per tile (fp32 partials,
+  // summed in split order by a second kernel) so that every CU gets a 256x256 tile
+  const int nk = (a.K + 63) / 64;
+  if (a.M >= 256 && a.N >= 256 && ((long)a.M * a.N) % 4 == 0) {
+    int S = (int)std::min<long>(8, (256 + big - 1) / big);
+    while (S > 1 && nk / S < kMinStepsPerSplit) --S;
+    if (S > 1) {
+      const long mn = (long)a.M * a.N;
+      std::lock_guard<std::mutex> lock(g_split_mutex);
+      float* ws = nullptr;
+      int rc = split_workspace((size_t)S * mn, &ws);
+      if (rc != QGEMM_OK) return rc;
+      a.ws = ws;
+      a.splits = S;
+      rc = launch_dense<FMT, 256, 256, 2, 4, 2>(a, wq, sc, s);
+      if (rc != QGEMM_OK) return rc;
+      const long n4 = mn / 4;
+      hipLaunchKernelGGL(qg::splitk_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, ws, a.y, n4, S,
+                         mn);
+      return check_launch("qgemm_dense split-K reduction");
+    }
+  }
   return launch_dense<FMT, 128, 128, 2, 2, 2>(a, wq, sc, s);
 }
 

@@ -156,4 +156,20 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   *reinterpret_cast<float4*>(out + t * N + n0) = acc;
 }
 
+// y[i] = sum_{s < splits} ws[s][i], summed in increasing s (deterministic); 4 floats per thread.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ ws, float* __restrict__ y,
+                                                            long n4, int splits, long stride) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  float4 acc = reinterpret_cast<const float4*>(ws)[i];
+  for (int s = 1; s < splits; ++s) {
+    const float4 v = reinterpret_cast<const float4*>(ws + (long)s * stride)[i];
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  reinterpret_cast<float4*>(y)[i] = acc;
+}
+
 }  // namespace qg

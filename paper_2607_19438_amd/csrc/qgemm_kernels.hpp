@@ -137,6 +137,10 @@ struct TileArgs {
   int n_experts;           // experts handled by this launch (<= kMaxExpertsPerLaunch)
   int topk;
   int T;
+  // dense split-K: `splits` workgroups share a tile, each over a contiguous range of K steps,
+  // writing fp32 partials to ws[split][M][N] (summed afterwards in split order)
+  float* ws;
+  int splits;
 };
 
 // Map a linear workgroup id to a tile id so that each XCD (workgroups are
@@ -204,7 +208,8 @@ template <int FMT, int BM, int BN, int WM, int WN, bool MOE, bool FULL, int XS>
 __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __restrict__ wq,
                                           const uint16_t* __restrict__ sc, int m0, int n0,
                                           int rows_valid, const int* __restrict__ s_xrow,
-                                          const int* __restrict__ s_yrow, char* __restrict__ lds_generic) {
+                                          const int* __restrict__ s_yrow, char* __restrict__ lds_generic,
+                                          int ks0, int nsteps, float* __restrict__ yout) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, MOE, XS>;
   constexpr int kUnitsPerChunk = (FMT == kQ8) ? 2 : 4;        // 16-byte LDS writes per 16-byte load
   constexpr int kUnits = KT::kWChunks * kUnitsPerChunk;        // per thread per K step
@@ -222,7 +227,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   const int wn = wave % WN;
   const int K = a.K;
   const int N = a.N;
-  const int nk = (K + kBK - 1) / kBK;
+  const int nk = nsteps;          // K steps of this workgroup: absolute steps ks0 .. ks0 + nk - 1
   const uint32_t kblocks = (uint32_t)K >> 5;
   const uint32_t wrow_bytes = (FMT == kQ8) ? (uint32_t)K : (uint32_t)K >> 1;
   const int n_valid = min(BN, N - n0);
@@ -271,7 +276,8 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     for (int u = 0; u < kUnitsPerChunk; ++u) lds_w[i][u] = lds_chunk(r, c * kUnitsPerChunk + u);
   }
 
-  auto issue_x = [&](int kt, int stage) {
+  auto issue_x = [&](int kt_local, int stage) {
+    const int kt = ks0 + kt_local;
     const uint32_t kbyte = (uint32_t)kt * (uint32_t)kRowBytes;
     const bool tail = (kt + 1) * kBK > K;
 #pragma unroll
@@ -286,7 +292,8 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   uint4 wv[2][KT::kWChunks];
   uint32_t sv[2][KT::kWChunks];
 
-  auto issue_w = [&](int kt, uint4 (&w)[KT::kWChunks], uint32_t (&s)[KT::kWChunks]) {
+  auto issue_w = [&](int kt_local, uint4 (&w)[KT::kWChunks], uint32_t (&s)[KT::kWChunks]) {
+    const int kt = ks0 + kt_local;
 #pragma unroll
     for (int i = 0; i < KT::kWChunks; ++i) {
       w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
@@ -302,7 +309,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     const int i = u / kUnitsPerChunk;
     const int sub = u % kUnitsPerChunk;
     if (sub == 0) {
-      const bool valid = kt * kBK + wcol[i] * KT::kWChunkElems < K;
+      const bool valid = (ks0 + kt) * kBK + wcol[i] * KT::kWChunkElems < K;
       scl[i] = valid ? fp16_to_f32((uint16_t)s[i]) : 0.0f;
       if constexpr (FMT == kQ4) {
         scl16[i] = scl[i] * 0.0625f;
@@ -476,7 +483,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       if (!FULL && row >= rows_valid) continue;
       const int dst = MOE ? s_yrow[row] : (m0 + row);
       if (MOE && dst < 0) continue;
-      float* yrow = a.y + (size_t)dst * N + n0 + wn * KT::kWTN + lr;
+      float* yrow = yout + (size_t)dst * N + n0 + wn * KT::kWTN + lr;
       if (full_cols) {
 #pragma unroll
         for (int j = 0; j < KT::kTN; ++j) yrow[j * 32] = acc[i][j][r];
@@ -493,11 +500,11 @@ template <int FMT, int BM, int BN, int WM, int WN, bool MOE, int XS>
 __device__ __forceinline__ void tile_dispatch(const TileArgs& a, const uint8_t* __restrict__ wq,
                                               const uint16_t* __restrict__ sc, int m0, int n0, int rows_valid,
                                               const int* __restrict__ s_xrow, const int* __restrict__ s_yrow,
-                                              char* __restrict__ lds) {
+                                              char* __restrict__ lds, int ks0, int nsteps, float* __restrict__ yout) {
   if (rows_valid == BM)
-    tile_body<FMT, BM, BN, WM, WN, MOE, true, XS>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds);
+    tile_body<FMT, BM, BN, WM, WN, MOE, true, XS>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0, nsteps, yout);
   else
-    tile_body<FMT, BM, BN, WM, WN, MOE, false, XS>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds);
+    tile_body<FMT, BM, BN, WM, WN, MOE, false, XS>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0, nsteps, yout);
 }
 
 template <int FMT, int BM, int BN, int WM, int WN, int XS>
@@ -508,13 +515,20 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
   const int mt_n = (a.M + BM - 1) / BM;
   const int nt_n = (a.N + BN - 1) / BN;
   const int ntiles = mt_n * nt_n;
-  const int tile = xcd_tile(blockIdx.x, ntiles);
+  const int split = (int)blockIdx.x / ntiles;
+  const int tile = xcd_tile((int)blockIdx.x - split * ntiles, ntiles);
   // column-tile major: consecutive tiles (same XCD) share a weight column tile
   const int nt = tile / mt_n;
   const int mt = tile - nt * mt_n;
   const int m0 = mt * BM;
   const int rows_valid = min(BM, a.M - m0);
-  tile_dispatch<FMT, BM, BN, WM, WN, false, XS>(a, wq, sc, m0, nt * BN, rows_valid, nullptr, nullptr, lds);
+  const int nk_all = (a.K + kBK - 1) / kBK;
+  const int per = (nk_all + a.splits - 1) / a.splits;
+  const int ks0 = split * per;
+  const int nsteps = min(per, nk_all - ks0);
+  float* yout = a.splits > 1 ? a.ws + (size_t)split * a.M * a.N : a.y;
+  tile_dispatch<FMT, BM, BN, WM, WN, false, XS>(a, wq, sc, m0, nt * BN, rows_valid, nullptr, nullptr, lds, ks0,
+                                                nsteps, yout);
 }
 
 // Grouped MoE GEMM: the launch covers experts [e_begin, e_begin + n_experts).
@@ -585,7 +599,8 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtr
     s_xrow[r] = asg < 0 ? -1 : asg / a.topk;
   }
   __syncthreads();
-  tile_dispatch<FMT, BM, BN, WM, WN, true, XS>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow, s_rowidx, lds);
+  tile_dispatch<FMT, BM, BN, WM, WN, true, XS>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow, s_rowidx, lds, 0,
+                                               (a.K + kBK - 1) / kBK, a.y);
 }
 
 }  // namespace qg

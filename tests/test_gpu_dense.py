@@ -63,6 +63,9 @@ RAGGED = [
     (255, 257, 288), (300, 1000, 32), (64, 64, 2048 + 32),
     (3857, 3684, 96),      # 256x256 tiles with ragged M and N tails
     (4096, 4096, 64),      # 256x256 tiles, exact
+    (300, 1000, 1536),     # split-K over 2 workgroups per 256x256 tile, ragged M and N
+    (1000, 700, 4096 + 32),  # split-K over 5, K tail inside the last split
+    (512, 512, 8192),      # split-K over 4 (the down-projection shape class)
 ]
 
 
@@ -105,6 +108,25 @@ def test_bitwise_deterministic_and_tile_independent(fmt):
     torch.cuda.synchronize()
     assert torch.equal(y1, y2)
     assert torch.equal(y1[:200], y3)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_split_k_bitwise_repeatable(fmt):
+    """Split-K partials are summed in split order: repeat runs are bitwise equal."""
+    torch = torch_or_skip()
+    import paper_2607_19438_amd as q
+    case = synth.dense_case("splitk", fmt, 1024, 1024, 4096, seed=8)
+    x = dev_x(torch, case.x)
+    wq, sc = dev_w(torch, case.w)
+    y1 = q.dense(x, wq, sc, fmt)
+    y2 = q.dense(x, wq, sc, fmt)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    rows = synth.rng_for(3).integers(0, 1024, 300)
+    cols = synth.rng_for(4).integers(0, 1024, 300)
+    exact = oracle.dense_entries(case.x, case.w.wq, case.w.scales, fmt, rows, cols)
+    rounded = oracle.dense_entries(case.x, case.w.wq, case.w.scales, fmt, rows, cols, bf16_weights=True)
+    check_levels("split-K 1024x1024x4096 (sampled)", y1.cpu().numpy()[rows, cols], exact, rounded, 4096, True)
 
 
 def test_unit_scale_q_one_gives_row_sums_on_gpu():
