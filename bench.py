@@ -6,8 +6,9 @@ One step is one pass of the whole path over the 2048+-token prefill workloads:
 * dense Q8 gate/up projection, M=2048 tokens, K=2048, N=8192;
 * dense Q8 down projection, M=2048, K=8192, N=2048;
 * MoE Q4 FFN, T=2048 tokens, E=128 experts, top-8 (uniform router logits):
-  bucket token slots by expert, gate/up grouped GEMM (K=2048, N=1536),
-  SiLU-gated activation, down grouped GEMM (K=768, N=2048), router-weighted combine;
+  bucket token slots by expert, gate/up grouped GEMM (K=2048, N=1536) with the
+  SiLU-gated activation fused into its epilogue (``--unfused``: fp32 gate/up output,
+  then a separate SwiGLU kernel), down grouped GEMM (K=768, N=2048), router-weighted combine;
 * the same MoE FFN at T=8192 with Zipf-skewed routing (groups of 0 to ~8000 rows).
 
 ``value`` = algorithmic GEMM FLOP per step (2*M*N*K per dense GEMM, 2*(T*topk)*N*K
@@ -47,6 +48,8 @@ def parse():
     ap.add_argument("--cpu-sample-seconds", type=float, default=15.0)
     ap.add_argument("--no-events", action="store_true",
                     help="time the step without per-launch events (then no roofline figure)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="MoE gate/up to fp32 then a separate SwiGLU kernel instead of the fused epilogue")
     ap.add_argument("--only", default="", help="comma list of parts to run: dense_gate_up,dense_down,moe_t2048,moe_t8192")
     return ap.parse_args()
 
@@ -57,7 +60,7 @@ class Part:
         self.flops = flops
 
 
-def build_parts(torch, q, synth, only):
+def build_parts(torch, q, synth, only, fused=True):
     """Device-resident inputs and output buffers for every part of the step."""
     dev = torch.device("cuda:0")
 
@@ -101,7 +104,8 @@ def build_parts(torch, q, synth, only):
         p.tgu = q.ExpertTable(p.wgu, p.sgu, case.fmt)
         p.td = q.ExpertTable(p.wd, p.sd, case.fmt)
         p.perm = torch.empty((A,), dtype=torch.int32, device=dev)
-        p.y1 = torch.empty((A, 2 * case.inter), dtype=torch.float32, device=dev)
+        p.fused = fused
+        p.y1 = None if fused else torch.empty((A, 2 * case.inter), dtype=torch.float32, device=dev)
         p.h = torch.empty((A, case.inter), dtype=torch.bfloat16, device=dev)
         p.y2 = torch.empty((A, case.hidden), dtype=torch.float32, device=dev)
         p.out = torch.empty((case.T, case.hidden), dtype=torch.float32, device=dev)
@@ -119,9 +123,13 @@ def run_part(q, p, timer=None):
         return
     c = p.case
     q.moe_bucket(p.idx, p.off, out=p.perm)
-    with timer(p.name + ":gate_up"):
-        q.moe_grouped(p.x, p.perm, p.off, p.tgu, None, c.topk, c.fmt, out=p.y1)
-    q.swiglu(p.y1, out=p.h)
+    if p.fused:
+        with timer(p.name + ":gate_up"):
+            q.moe_gate_up_swiglu(p.x, p.perm, p.off, p.tgu, None, c.topk, c.fmt, out=p.h)
+    else:
+        with timer(p.name + ":gate_up"):
+            q.moe_grouped(p.x, p.perm, p.off, p.tgu, None, c.topk, c.fmt, out=p.y1)
+        q.swiglu(p.y1, out=p.h)
     with timer(p.name + ":down"):
         q.moe_grouped(p.h, p.perm, p.off, p.td, None, 1, c.fmt, out=p.y2)
     q.moe_combine(p.y2, p.rw, c.topk, out=p.out)
@@ -236,7 +244,7 @@ def main():
     q.lib()
     log("generating inputs")
     t0 = time.perf_counter()
-    parts = build_parts(torch, q, synth, args.only)
+    parts = build_parts(torch, q, synth, args.only, fused=not args.unfused)
     torch.cuda.synchronize()
     log(f"inputs resident in HBM ({time.perf_counter() - t0:.1f} s)")
     plain = EventTimer(torch, False)
@@ -299,6 +307,7 @@ def main():
         "config": {"workload": "prefill_2048: dense Q8 gate_up 2048x8192x2048 + dense Q8 down 2048x2048x8192 + "
                                "MoE Q4 FFN T=2048 E=128 top8 + MoE Q4 FFN T=8192 E=128 top8 Zipf-skewed"
                                if not args.only else args.only,
+                   "moe_swiglu": "separate kernel" if args.unfused else "fused into gate/up epilogue",
                    "frac_of_mfma_peak": value / PEAK_BF16_TFLOPS, "flop_per_step": flops_step},
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -13,7 +13,8 @@
  * - Pointers are DEVICE pointers (memory the HIP runtime of this process
  *   allocated on the current device) unless the comment says HOST.
  * - Arrays are dense and row-major; no strides. Every device pointer must be
- *   16-byte aligned (QGEMM_EALIGN otherwise).
+ *   16-byte aligned, except fp16 scale arrays, which need 2-byte alignment
+ *   (QGEMM_EALIGN otherwise).
  * - Work is enqueued on `stream` (0 = the null stream) and the call returns
  *   without synchronising; device faults surface at the caller's next sync.
  *   The caller keeps every buffer alive until the stream has passed the call.
@@ -65,6 +66,10 @@ enum qgemm_status {
  * x: bf16 [M][K]; wq: int8 [N][K] (Q8) or uint8 [N][K/2] (Q4);
  * scales: fp16 [N][K/32]; y: fp32 [M][N].
  * Sizes: M >= 0, 1 <= N, 32 <= K, K % 32 == 0, every element count < 2^31.
+ * When few output tiles meet a long K, the call splits K over several
+ * workgroups and sums their fp32 partials in split order (deterministic) in a
+ * library-owned workspace (grown on first use, freed by qgemm_release);
+ * concurrent calls on different streams must not share it.
  */
 int qgemm_dense(const void* x, const void* wq, const void* scales, float* y,
                 int M, int N, int K, int fmt, hipStream_t stream);
@@ -81,7 +86,7 @@ int qgemm_dense(const void* x, const void* wq, const void* scales, float* y,
  * wq, scales: HOST arrays of E device pointers, each laid out as for
  *   qgemm_dense with the same N and K.
  * y: fp32 [T*topk][N], in assignment (token-slot) order.
- * Sizes: 1 <= E <= 65536, 1 <= topk <= E, T*topk < 2^31.
+ * Sizes: 1 <= E <= 4096, 1 <= topk <= E, T*topk < 2^31, T*K < 2^31.
  * The call buckets the assignments by expert into a library-owned workspace
  * (grown on first use, then reused; freed by qgemm_release) and runs the
  * grouped GEMM. Routing tables that disagree with each other are a caller
@@ -116,6 +121,29 @@ int qgemm_moe_grouped(const void* x, const int32_t* perm, const int32_t* expert_
                       int T, int E, int topk, int N, int K, int fmt, hipStream_t stream);
 
 /*
+ * Fused MoE gate/up projection with the SiLU-gated activation in its epilogue
+ * (Section 3.1, fused gate/up item): for every assignment a routed to expert e
+ * (perm and expert_offsets as for qgemm_moe_grouped) and i < inter,
+ *   g = (dequant(wq[e], scales[e]) . x[a / topk])[i]
+ *   u = (dequant(wq[e], scales[e]) . x[a / topk])[inter + i]
+ *   h[a][i] = bf16_rne(silu(g) * u)
+ * with g and u the same fp32 values qgemm_moe_grouped writes to y[a][i] and
+ * y[a][inter + i], and silu evaluated as in qgemm_swiglu, so h equals
+ * qgemm_swiglu applied to qgemm_moe_grouped's output bit for bit; the fp32
+ * [T*topk][2*inter] intermediate is never stored.
+ * wq[e], scales[e]: the gate rows (0 .. inter-1) and then the up rows
+ * (inter .. 2*inter-1) of one [2*inter][K] matrix per expert, laid out as for
+ * qgemm_dense with N = 2*inter; each matrix spans less than 4 GiB.
+ * h: bf16 [T*topk][inter] in assignment order; rows of assignments absent
+ * from perm are not written.
+ * Sizes as for qgemm_moe with N = 2*inter, inter >= 1.
+ */
+int qgemm_moe_gate_up_swiglu(const void* x, const int32_t* perm, const int32_t* expert_offsets,
+                             const void* const* wq, const void* const* scales, void* h,
+                             int T, int E, int topk, int inter, int K, int fmt,
+                             hipStream_t stream);
+
+/*
  * SiLU-gated activation between the MoE projections (Section 3.1, fused
  * gate/up item): for r < rows, i < inter,
  *   h[r][i] = bf16_rne(silu(y1[r][i]) * y1[r][inter + i]),  silu(z) = z / (1 + e^-z)
@@ -135,8 +163,9 @@ int qgemm_moe_combine(const float* y2, const float* route_w, float* out,
 /* Message of the last non-OK return on the calling thread ("" if none). */
 const char* qgemm_last_error(void);
 
-/* Frees the library-owned MoE workspace (the next qgemm_moe grows it again).
- * The caller must have synchronised every stream that used it. */
+/* Frees the library-owned workspaces (MoE bucketing, split-K partials); the
+ * next call that needs one grows it again. The caller must have synchronised
+ * every stream that used them. */
 int qgemm_release(void);
 
 /* Library ABI version, (major << 16) | minor. */

@@ -16,7 +16,7 @@ import os
 import torch  # imported before the library so that both share one HIP runtime
 
 __all__ = ["Q8", "Q4", "QGemmError", "lib", "lib_path", "dense", "moe", "moe_bucket", "moe_grouped",
-           "swiglu", "moe_combine", "last_error", "release", "version", "EXPORTS", "ExpertTable"]
+           "moe_gate_up_swiglu", "swiglu", "moe_combine", "last_error", "release", "version", "EXPORTS", "ExpertTable"]
 
 Q8 = 0
 Q4 = 1
@@ -31,6 +31,7 @@ EXPORTS = {
     "qgemm_moe": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "qgemm_moe_bucket": (_i, [_vp, _vp, _vp, _i, _i, _vp]),
     "qgemm_moe_grouped": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "qgemm_moe_gate_up_swiglu": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "qgemm_swiglu": (_i, [_vp, _vp, _i, _i, _vp]),
     "qgemm_moe_combine": (_i, [_vp, _vp, _vp, _i, _i, _i, _vp]),
     "qgemm_last_error": (ctypes.c_char_p, []),
@@ -228,6 +229,30 @@ def moe_grouped(x, perm, expert_offsets, wq, scales, topk: int, fmt: int, out=No
     _need(out, "out", (torch.float32,), 2)
     _check(lib().qgemm_moe_grouped(x.data_ptr(), perm.data_ptr(), expert_offsets.data_ptr(), wp, sp,
                                    out.data_ptr(), T, E, topk, N, K, fmt, _stream(x)))
+    return out
+
+
+def moe_gate_up_swiglu(x, perm, expert_offsets, wq, scales, topk: int, fmt: int, out=None):
+    """Fused gate/up projection + SiLU gate (``qgemm_moe_gate_up_swiglu``): bf16 ``h[T*topk][inter]``.
+
+    Expert weights are ``[2*inter][K]`` (gate rows, then up rows); ``wq`` may be an ExpertTable."""
+    _need(x, "x", (torch.bfloat16,), 2)
+    _need(perm, "perm", (torch.int32,), 1)
+    _need(expert_offsets, "expert_offsets", (torch.int32,), 1)
+    T, K = x.shape
+    E = expert_offsets.shape[0] - 1
+    wq, scales, wp, sp = _expert_tables(wq, scales, E)
+    N = wq[0].shape[0]
+    if N % 2 != 0:
+        raise ValueError("gate/up weights need an even number of rows")
+    inter = N // 2
+    if out is None:
+        out = torch.empty((T * topk, inter), dtype=torch.bfloat16, device=x.device)
+    _need(out, "out", (torch.bfloat16,), 2)
+    if out.shape != (T * topk, inter):
+        raise ValueError("out must be [T*topk][inter]")
+    _check(lib().qgemm_moe_gate_up_swiglu(x.data_ptr(), perm.data_ptr(), expert_offsets.data_ptr(), wp, sp,
+                                          out.data_ptr(), T, E, topk, inter, K, fmt, _stream(x)))
     return out
 
 

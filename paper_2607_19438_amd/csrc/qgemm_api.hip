@@ -119,9 +119,9 @@ int dense_dispatch(qg::TileArgs a, const void* wq, const void* sc, hipStream_t s
   return launch_dense<FMT, 128, 128, 2, 2, 2>(a, wq, sc, s);
 }
 
-template <int FMT, int BM, int BN, int WM, int WN, int XS>
+template <int FMT, int BM, int BN, int WM, int WN, int XS, bool SWI>
 int launch_moe_cfg(qg::TileArgs a, const void* const* wq, const void* const* sc, int E, hipStream_t s) {
-  const int nt = (a.N + BN - 1) / BN;
+  const int nt = SWI ? (a.swi_inter + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
   for (int e0 = 0; e0 < E; e0 += qg::kMaxExpertsPerLaunch) {
     const int ne = (E - e0) < qg::kMaxExpertsPerLaunch ? (E - e0) : qg::kMaxExpertsPerLaunch;
     qg::ExpertPtrs ep;
@@ -136,7 +136,8 @@ int launch_moe_cfg(qg::TileArgs a, const void* const* wq, const void* const* sc,
     const long mt_bound = (long)(a.M + BM - 1) / BM + ne;
     const long grid = mt_bound * nt;
     if (grid > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "too many tiles");
-    hipLaunchKernelGGL((qg::moe_kernel<FMT, BM, BN, WM, WN, XS>), dim3((unsigned)grid), dim3(WM * WN * 64), 0, s, a, ep);
+    hipLaunchKernelGGL((qg::moe_kernel<FMT, BM, BN, WM, WN, XS, SWI>), dim3((unsigned)grid), dim3(WM * WN * 64), 0, s,
+                       a, ep);
     const int rc = check_launch("qgemm_moe");
     if (rc != QGEMM_OK) return rc;
   }
@@ -145,11 +146,11 @@ int launch_moe_cfg(qg::TileArgs a, const void* const* wq, const void* const* sc,
 
 // Tile height from the mean rows per expert (the host does not see the routing): groups of
 // about 100-200 rows fit one 192-row tile each; larger groups use 256-row tiles.
-template <int FMT>
+template <int FMT, bool SWI = false>
 int launch_moe(qg::TileArgs a, const void* const* wq, const void* const* sc, int E, hipStream_t s) {
   const long mean_rows = (long)a.M / E;
-  if (mean_rows > 192) return launch_moe_cfg<FMT, 256, 256, 2, 4, 2>(a, wq, sc, E, s);
-  return launch_moe_cfg<FMT, 192, 256, 2, 4, 2>(a, wq, sc, E, s);
+  if (mean_rows > 192) return launch_moe_cfg<FMT, 256, 256, 2, 4, 2, SWI>(a, wq, sc, E, s);
+  return launch_moe_cfg<FMT, 192, 256, 2, 4, 2, SWI>(a, wq, sc, E, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -332,6 +333,35 @@ int qgemm_moe_grouped(const void* x, const int32_t* perm, const int32_t* expert_
   return rc == QGEMM_OK ? ok() : rc;
 }
 
+int qgemm_moe_gate_up_swiglu(const void* x, const int32_t* perm, const int32_t* expert_offsets,
+                              const void* const* wq, const void* const* scales, void* h, int T, int E, int topk,
+                              int inter, int K, int fmt, hipStream_t stream) {
+  if (inter < 1 || inter > 0x3fffffff) return fail(QGEMM_EINVAL, "inter must be >= 1 (got %d)", inter);
+  if ((long)T * topk * inter > 0x7fffffffffffL) return fail(QGEMM_EUNSUPPORTED, "problem too large");
+  // the y pointer check of the shared validation stands for h
+  int rc = moe_args_check(x, perm, expert_offsets, wq, scales, static_cast<const float*>(h), T, E, topk, 2 * inter, K,
+                          fmt);
+  if (rc != QGEMM_OK || T == 0) return rc == QGEMM_OK ? ok() : rc;
+  if ((long)2 * inter * (K / 32) * 2 > 0xffffffffL || (long)2 * inter * K > 0xffffffffL)
+    return fail(QGEMM_EUNSUPPORTED, "an expert's weights span 4 GiB or more");
+  (void)hipGetLastError();
+  qg::TileArgs a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.y = nullptr;
+  a.M = T * topk;
+  a.N = 2 * inter;
+  a.K = K;
+  a.perm = perm;
+  a.offsets = expert_offsets;
+  a.topk = topk;
+  a.T = T;
+  a.swi_inter = inter;
+  a.h = static_cast<uint16_t*>(h);
+  rc = (fmt == QGEMM_Q8) ? launch_moe<qg::kQ8, true>(a, wq, scales, E, stream)
+                         : launch_moe<qg::kQ4, true>(a, wq, scales, E, stream);
+  return rc == QGEMM_OK ? ok() : rc;
+}
+
 int qgemm_moe(const void* x, const int32_t* token_expert_idx, const int32_t* expert_offsets, const void* const* wq,
               const void* const* scales, float* y, int T, int E, int topk, int N, int K, int fmt,
               hipStream_t stream) {
@@ -433,6 +463,15 @@ int qgemm_release(void) {
     if (w.counts) (void)hipFree(w.counts);
     if (w.flag) (void)hipFree(w.flag);
     w = Workspace{};
+  }
+  {
+    std::lock_guard<std::mutex> split_lock(g_split_mutex);
+    for (size_t d = 0; d < g_split_ws.size(); ++d) {
+      if (!g_split_ws[d].first) continue;
+      (void)hipSetDevice((int)d);
+      (void)hipFree(g_split_ws[d].first);
+      g_split_ws[d] = {nullptr, 0};
+    }
   }
   (void)hipSetDevice(cur);
   (void)hipGetLastError();

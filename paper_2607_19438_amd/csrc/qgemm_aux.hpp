@@ -128,8 +128,8 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ y
   uint32_t o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const float a0 = g[2 * i] / (1.0f + __expf(-g[2 * i])) * u[2 * i];
-    const float a1 = g[2 * i + 1] / (1.0f + __expf(-g[2 * i + 1])) * u[2 * i + 1];
+    const float a0 = swiglu_f32(g[2 * i], u[2 * i]);
+    const float a1 = swiglu_f32(g[2 * i + 1], u[2 * i + 1]);
     o[i] = pack_bf16x2(a0, a1);
   }
   *reinterpret_cast<uint4*>(h + r * inter + i0) = make_uint4(o[0], o[1], o[2], o[3]);

@@ -80,6 +80,10 @@ __device__ __forceinline__ void dequant_q4x32(const uint4 w, float s, uint32_t o
   }
 }
 
+// h = silu(g) * u in fp32 (the SiLU-gated activation); shared by the fused epilogue and the
+// standalone kernel so both round the same fp32 value to bf16.
+__device__ __forceinline__ float swiglu_f32(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
+
 // One 16-byte LDS unit of dequantised weights = 8 bf16.
 // Q8: two dwords of int8 (8 weights) with scale s.
 __device__ __forceinline__ u32x4 dequant_q8_unit(uint32_t d0, uint32_t d1, float s) {
@@ -141,6 +145,9 @@ struct TileArgs {
   // writing fp32 partials to ws[split][M][N] (summed afterwards in split order)
   float* ws;
   int splits;
+  // fused SwiGLU epilogue (MoE gate/up): N = 2 * swi_inter weight rows, h is bf16 [rows][swi_inter]
+  int swi_inter;
+  uint16_t* h;
 };
 
 // Map a linear workgroup id to a tile id so that each XCD (workgroups are
@@ -204,13 +211,14 @@ constexpr int kSchedDSWrite = 0x200;
 //   (kt+1)&1) interleaved between them
 //   wait for the activation DMA and the LDS writes, then barrier
 // FULL: every row of the tile is valid, so no MFMA is skipped (branch-free body).
-template <int FMT, int BM, int BN, int WM, int WN, bool MOE, bool FULL, int XS>
+template <int FMT, int BM, int BN, int WM, int WN, bool MOE, bool FULL, int XS, bool SWI>
 __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __restrict__ wq,
                                           const uint16_t* __restrict__ sc, int m0, int n0,
                                           int rows_valid, const int* __restrict__ s_xrow,
                                           const int* __restrict__ s_yrow, char* __restrict__ lds_generic,
                                           int ks0, int nsteps, float* __restrict__ yout) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, MOE, XS>;
+  static_assert(!SWI || MOE, "the fused SwiGLU epilogue is a MoE gate/up epilogue");
   constexpr int kUnitsPerChunk = (FMT == kQ8) ? 2 : 4;        // 16-byte LDS writes per 16-byte load
   constexpr int kUnits = KT::kWChunks * kUnitsPerChunk;        // per thread per K step
   static_assert(kUnits % 4 == 0, "units must spread evenly over the four K16 sub-steps");
@@ -258,20 +266,36 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     }
   }
   // --- weight / scale offsets of this thread's chunks ---
-  const __amdgpu_buffer_rsrc_t wr = make_rsrc(wq + (size_t)n0 * wrow_bytes, (uint32_t)n_valid * wrow_bytes);
-  const __amdgpu_buffer_rsrc_t sr = make_rsrc(sc + (size_t)n0 * kblocks, (uint32_t)n_valid * kblocks * 2u);
+  // Weight rows of the tile: rows n0 .. n0 + BN - 1, or for the fused SwiGLU epilogue gate/up
+  // pairs, tile row 2j -> gate row h0 + j and 2j + 1 -> up row inter + h0 + j (h0 = n0 / 2), so
+  // each gate/up pair sits in two neighbouring MFMA columns (lanes). Rows past the matrix read
+  // row 0 with a zero scale (SwiGLU) or fall outside the buffer range (plain).
+  const int swi_inter = a.swi_inter;
+  const int h0 = n0 >> 1;
+  const __amdgpu_buffer_rsrc_t wr =
+      SWI ? make_rsrc(wq, (uint32_t)N * wrow_bytes) : make_rsrc(wq + (size_t)n0 * wrow_bytes, (uint32_t)n_valid * wrow_bytes);
+  const __amdgpu_buffer_rsrc_t sr = SWI ? make_rsrc(sc, (uint32_t)N * kblocks * 2u)
+                                        : make_rsrc(sc + (size_t)n0 * kblocks, (uint32_t)n_valid * kblocks * 2u);
   uint32_t woff[KT::kWChunks];
   uint32_t soff[KT::kWChunks];
   int lds_w[KT::kWChunks][kUnitsPerChunk];   // LDS byte offset (within the W tile) of each unit
   int wcol[KT::kWChunks];
+  bool wrow_ok[KT::kWChunks];
 #pragma unroll
   for (int i = 0; i < KT::kWChunks; ++i) {
     const int q = tid + i * KT::kThreads;
     const int r = q / KT::kWChunksPerRow;
     const int c = q % KT::kWChunksPerRow;
+    int grow = r;
+    wrow_ok[i] = true;
+    if constexpr (SWI) {
+      const int hc = h0 + (r >> 1);
+      wrow_ok[i] = hc < swi_inter;
+      grow = wrow_ok[i] ? ((r & 1) ? swi_inter + hc : hc) : 0;
+    }
     wcol[i] = c;
-    woff[i] = (uint32_t)r * wrow_bytes + (uint32_t)c * 16u;
-    soff[i] = ((uint32_t)r * kblocks + (uint32_t)(c * KT::kWChunkElems / 32)) * 2u;
+    woff[i] = (uint32_t)grow * wrow_bytes + (uint32_t)c * 16u;
+    soff[i] = ((uint32_t)grow * kblocks + (uint32_t)(c * KT::kWChunkElems / 32)) * 2u;
 #pragma unroll
     for (int u = 0; u < kUnitsPerChunk; ++u) lds_w[i][u] = lds_chunk(r, c * kUnitsPerChunk + u);
   }
@@ -309,7 +333,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     const int i = u / kUnitsPerChunk;
     const int sub = u % kUnitsPerChunk;
     if (sub == 0) {
-      const bool valid = (ks0 + kt) * kBK + wcol[i] * KT::kWChunkElems < K;
+      const bool valid = wrow_ok[i] && (ks0 + kt) * kBK + wcol[i] * KT::kWChunkElems < K;
       scl[i] = valid ? fp16_to_f32((uint16_t)s[i]) : 0.0f;
       if constexpr (FMT == kQ4) {
         scl16[i] = scl[i] * 0.0625f;
@@ -473,6 +497,33 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   }
 
   // --- epilogue: lane holds column (lane & 31) and rows (r/4)*8 + (lane/32)*4 + r%4 of each block ---
+  if constexpr (SWI) {
+    // lanes 2k (gate) and 2k + 1 (up) hold the pair of h column h0 + (tile column) / 2; both lanes
+    // of a pair share the row, so they are active together around the exchange
+#pragma unroll
+    for (int i = 0; i < KT::kTM; ++i) {
+      if (!FULL && i >= mblocks) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = (i * WM + wm) * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+        if (!FULL && row >= rows_valid) continue;
+        const int dst = s_yrow[row];
+        if (dst < 0) continue;
+        uint16_t* hrow = a.h + (size_t)dst * swi_inter;
+#pragma unroll
+        for (int j = 0; j < KT::kTN; ++j) {
+          const float v = acc[i][j][r];
+          // DPP quad_perm [1,0,3,2]: the value of lane l ^ 1
+          const float partner = __builtin_bit_cast(
+              float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+          const int hc = h0 + ((wn * KT::kWTN + j * 32 + lr) >> 1);
+          if ((lr & 1) == 0 && hc < swi_inter)
+            hrow[hc] = (uint16_t)(pack_bf16x2(swiglu_f32(v, partner), 0.0f) & 0xFFFFu);
+        }
+      }
+    }
+    return;
+  }
   const bool full_cols = n0 + BN <= N;
 #pragma unroll
   for (int i = 0; i < KT::kTM; ++i) {
@@ -496,15 +547,17 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   }
 }
 
-template <int FMT, int BM, int BN, int WM, int WN, bool MOE, int XS>
+template <int FMT, int BM, int BN, int WM, int WN, bool MOE, int XS, bool SWI>
 __device__ __forceinline__ void tile_dispatch(const TileArgs& a, const uint8_t* __restrict__ wq,
                                               const uint16_t* __restrict__ sc, int m0, int n0, int rows_valid,
                                               const int* __restrict__ s_xrow, const int* __restrict__ s_yrow,
                                               char* __restrict__ lds, int ks0, int nsteps, float* __restrict__ yout) {
   if (rows_valid == BM)
-    tile_body<FMT, BM, BN, WM, WN, MOE, true, XS>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0, nsteps, yout);
+    tile_body<FMT, BM, BN, WM, WN, MOE, true, XS, SWI>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0, nsteps,
+                                                       yout);
   else
-    tile_body<FMT, BM, BN, WM, WN, MOE, false, XS>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0, nsteps, yout);
+    tile_body<FMT, BM, BN, WM, WN, MOE, false, XS, SWI>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0, nsteps,
+                                                        yout);
 }
 
 template <int FMT, int BM, int BN, int WM, int WN, int XS>
@@ -527,15 +580,15 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
   const int ks0 = split * per;
   const int nsteps = min(per, nk_all - ks0);
   float* yout = a.splits > 1 ? a.ws + (size_t)split * a.M * a.N : a.y;
-  tile_dispatch<FMT, BM, BN, WM, WN, false, XS>(a, wq, sc, m0, nt * BN, rows_valid, nullptr, nullptr, lds, ks0,
-                                                nsteps, yout);
+  tile_dispatch<FMT, BM, BN, WM, WN, false, XS, false>(a, wq, sc, m0, nt * BN, rows_valid, nullptr, nullptr, lds, ks0,
+                                                       nsteps, yout);
 }
 
 // Grouped MoE GEMM: the launch covers experts [e_begin, e_begin + n_experts).
 // Work items are (expert, m tile, n tile) over active experts only; every
 // workgroup decodes its item from the per-expert counts, so the host never
 // needs the routing.
-template <int FMT, int BM, int BN, int WM, int WN, int XS>
+template <int FMT, int BM, int BN, int WM, int WN, int XS, bool SWI>
 __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtrs ep) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, true, XS>;
   static_assert(KT::kThreads >= kMaxExpertsPerLaunch, "the tile prefix needs one lane per expert");
@@ -544,7 +597,8 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtr
   __shared__ int s_rowidx[BM];   // y row (assignment) of each tile row
   __shared__ int s_xrow[BM];     // x row (token = assignment / topk) of each tile row
   const int tid = threadIdx.x;
-  const int nt_n = (a.N + BN - 1) / BN;
+  // fused SwiGLU: a tile covers BN / 2 columns of h (BN interleaved gate/up weight rows)
+  const int nt_n = SWI ? (a.swi_inter + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
   const int ne = a.n_experts;
 
   // per-expert tile counts -> inclusive prefix over the launch's experts (<= 128):
@@ -599,8 +653,8 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtr
     s_xrow[r] = asg < 0 ? -1 : asg / a.topk;
   }
   __syncthreads();
-  tile_dispatch<FMT, BM, BN, WM, WN, true, XS>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow, s_rowidx, lds, 0,
-                                               (a.K + kBK - 1) / kBK, a.y);
+  tile_dispatch<FMT, BM, BN, WM, WN, true, XS, SWI>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow, s_rowidx,
+                                                    lds, 0, (a.K + kBK - 1) / kBK, a.y);
 }
 
 }  // namespace qg

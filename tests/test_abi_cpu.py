@@ -32,7 +32,7 @@ def header_prototypes():
 
 def test_header_declares_the_boundary():
     p = header_prototypes()
-    for name in ("qgemm_dense", "qgemm_moe", "qgemm_moe_bucket", "qgemm_moe_grouped", "qgemm_swiglu",
+    for name in ("qgemm_dense", "qgemm_moe", "qgemm_moe_bucket", "qgemm_moe_grouped", "qgemm_moe_gate_up_swiglu", "qgemm_swiglu",
                  "qgemm_moe_combine", "qgemm_last_error", "qgemm_release", "qgemm_version"):
         assert name in p
 
@@ -83,6 +83,10 @@ def test_moe_host_validation(qmod):
     assert lib.qgemm_moe(16, 16, 16, ptrs, ptrs, 16, 0, 4, 2, 128, 64, 0, None) == 0       # T == 0
     assert lib.qgemm_moe(0, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 128, 64, 0, None) == -1       # null x
     assert lib.qgemm_moe_grouped(16, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 128, 64, 9, None) == -1
+    assert lib.qgemm_moe_gate_up_swiglu(16, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 0, 64, 0, None) == -1   # inter < 1
+    assert lib.qgemm_moe_gate_up_swiglu(16, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 64, 48, 0, None) == -1  # K % 32
+    assert lib.qgemm_moe_gate_up_swiglu(16, 16, 16, ptrs, ptrs, 16, 0, 4, 2, 64, 64, 0, None) == 0   # T == 0
+    assert lib.qgemm_moe_gate_up_swiglu(16, 16, 16, ptrs, ptrs, 18, 4, 4, 2, 64, 64, 0, None) == -2  # h misaligned
     assert lib.qgemm_moe_bucket(16, 16, 16, -1, 4, None) == -1
     assert lib.qgemm_moe_bucket(16, 16, 16, 0, 4, None) == 0
     assert lib.qgemm_swiglu(16, 16, 4, 12, None) == -1
