@@ -50,6 +50,8 @@ def parse():
                     help="time the step without per-launch events (then no roofline figure)")
     ap.add_argument("--unfused", action="store_true",
                     help="MoE gate/up to fp32 then a separate SwiGLU kernel instead of the fused epilogue")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB three times (for scaling HBM byte counters) and exit")
     ap.add_argument("--only", default="", help="comma list of parts to run: dense_gate_up,dense_down,moe_t2048,moe_t8192")
     return ap.parse_args()
 
@@ -236,11 +238,21 @@ def main():
         log("only --gpus 1 is supported: the path is a single-GPU kernel library")
         return 2
     import torch
-    import paper_2607_19438_amd as q
-    import synth
     if not torch.cuda.is_available():
         log("no GPU visible")
         return 1
+    if args.copy_calibration:
+        # a plain device-to-device copy of a known size: the reference reading for HBM byte counters
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copied {n * 4} bytes three times")
+        return 0
+    import paper_2607_19438_amd as q
+    import synth
     q.lib()
     log("generating inputs")
     t0 = time.perf_counter()

@@ -498,27 +498,32 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
 
   // --- epilogue: lane holds column (lane & 31) and rows (r/4)*8 + (lane/32)*4 + r%4 of each block ---
   if constexpr (SWI) {
-    // lanes 2k (gate) and 2k + 1 (up) hold the pair of h column h0 + (tile column) / 2; both lanes
-    // of a pair share the row, so they are active together around the exchange
+    // Lanes 2k (gate) and 2k + 1 (up) hold the pair of h column h0 + (tile column) / 2 for the
+    // same 16 rows. One exchange per row pair splits the work: the even lane keeps rows q
+    // (0 <= q < 8) and receives their up values, the odd lane keeps rows q + 8 and receives their
+    // gate values, so every lane evaluates the SiLU gate for 8 rows and stores them.
+    const bool odd = (lr & 1) != 0;
 #pragma unroll
     for (int i = 0; i < KT::kTM; ++i) {
       if (!FULL && i >= mblocks) continue;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = (i * WM + wm) * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
-        if (!FULL && row >= rows_valid) continue;
-        const int dst = s_yrow[row];
-        if (dst < 0) continue;
-        uint16_t* hrow = a.h + (size_t)dst * swi_inter;
+      for (int j = 0; j < KT::kTN; ++j) {
+        const int hc = h0 + ((wn * KT::kWTN + j * 32 + lr) >> 1);
 #pragma unroll
-        for (int j = 0; j < KT::kTN; ++j) {
-          const float v = acc[i][j][r];
-          // DPP quad_perm [1,0,3,2]: the value of lane l ^ 1
-          const float partner = __builtin_bit_cast(
-              float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
-          const int hc = h0 + ((wn * KT::kWTN + j * 32 + lr) >> 1);
-          if ((lr & 1) == 0 && hc < swi_inter)
-            hrow[hc] = (uint16_t)(pack_bf16x2(swiglu_f32(v, partner), 0.0f) & 0xFFFFu);
+        for (int q = 0; q < 8; ++q) {
+          const float lo = acc[i][j][q];
+          const float hi = acc[i][j][q + 8];
+          // DPP quad_perm [1,0,3,2]: the value of lane l ^ 1 (both lanes active)
+          const float recv = __builtin_bit_cast(
+              float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, odd ? lo : hi), 0xB1, 0xF, 0xF, false));
+          const float g = odd ? recv : lo;
+          const float u = odd ? hi : recv;
+          const int rm = odd ? q + 8 : q;
+          const int row = (i * WM + wm) * 32 + (rm >> 2) * 8 + lh * 4 + (rm & 3);
+          if (!FULL && row >= rows_valid) continue;
+          const int dst = s_yrow[row];
+          if (dst >= 0 && hc < swi_inter)
+            a.h[(size_t)dst * swi_inter + hc] = (uint16_t)(pack_bf16x2(swiglu_f32(g, u), 0.0f) & 0xFFFFu);
         }
       }
     }
