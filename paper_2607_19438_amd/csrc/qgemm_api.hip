@@ -131,10 +131,10 @@ int launch_moe_cfg(qg::TileArgs a, const void* const* wq, const void* const* sc,
     }
     a.e_begin = e0;
     a.n_experts = ne;
-    // upper bound of sum_e ceil(c_e / BM) over the launch's experts; workgroups past the
-    // real tile count exit at once
+    // upper bound of sum_e ceil(c_e / BM) over the launch's experts (m-tile groups), rounded up
+    // to the 8 XCDs; workgroups past the real group count exit at once
     const long mt_bound = (long)(a.M + BM - 1) / BM + ne;
-    const long grid = mt_bound * nt;
+    const long grid = (mt_bound + 7) / 8 * 8 * nt;
     if (grid > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "too many tiles");
     hipLaunchKernelGGL((qg::moe_kernel<FMT, BM, BN, WM, WN, XS, SWI>), dim3((unsigned)grid), dim3(WM * WN * 64), 0, s,
                        a, ep);

@@ -606,20 +606,19 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtr
   const int nt_n = SWI ? (a.swi_inter + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
   const int ne = a.n_experts;
 
-  // per-expert tile counts -> inclusive prefix over the launch's experts (<= 128):
+  // per-expert m-tile counts -> inclusive prefix over the launch's experts (<= 128):
   // one expert per lane of the first two waves, wave prefix sums, then combine.
   __shared__ int s_wsum[2];
   if (tid < 128) {
-    int tiles = 0;
+    int mtiles = 0;
     if (tid < ne) {
       const int lo = a.offsets[a.e_begin + tid];
       const int hi = a.offsets[a.e_begin + tid + 1];
       int c = hi - lo;
       if (lo < 0 || hi > a.M || c < 0) c = 0;   // inconsistent table: no work for this expert
-      const long t = ((long)c + BM - 1) / BM * nt_n;
-      tiles = (int)(t < (1L << 23) ? t : (1L << 23));   // keeps the sum of 128 experts below 2^31
+      mtiles = (c + BM - 1) / BM;
     }
-    int incl = tiles;
+    int incl = mtiles;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
       const int v = __shfl_up(incl, d, 64);
@@ -632,19 +631,26 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtr
   __syncthreads();
   if (tid >= 64 && tid < 128) s_prefix[tid + 1] += s_wsum[0];
   __syncthreads();
-  const int ntiles = s_prefix[ne];
-  if ((int)blockIdx.x >= ntiles) return;
-  const int tile = xcd_tile(blockIdx.x, ntiles);
-  // largest e with s_prefix[e] <= tile
+  // Work unit: an m-tile group = one expert's BM gathered rows against all nt_n column tiles.
+  // Workgroups reach the 8 XCDs round-robin (bid % 8); XCD x takes groups x, x + 8, x + 16, ...
+  // with a group's column tiles consecutive, so the group's gathered rows and an expert's
+  // weights are shared through that XCD's L2, while heavy and light groups (skewed routing)
+  // spread evenly over the XCDs. The host sizes the grid as 8 * ceil(groups bound / 8) * nt_n.
+  const int ngroups = s_prefix[ne];
+  const int xcd = (int)blockIdx.x & 7;
+  const int local = (int)blockIdx.x >> 3;
+  const int gl = local / nt_n;
+  const int nt = local - gl * nt_n;
+  const int g = xcd + 8 * gl;
+  if (g >= ngroups) return;
+  // largest e with s_prefix[e] <= g
   int lo = 0, hi = ne;
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
-    if (s_prefix[mid] <= tile) lo = mid; else hi = mid;
+    if (s_prefix[mid] <= g) lo = mid; else hi = mid;
   }
   const int e = lo;
-  const int local = tile - s_prefix[e];
-  const int mt = local / nt_n;           // m-tile major: consecutive tiles share the gathered rows
-  const int nt = local - mt * nt_n;
+  const int mt = g - s_prefix[e];
   const int pbeg = a.offsets[a.e_begin + e] + mt * BM;
   const int pend = a.offsets[a.e_begin + e + 1];
   const int rows_valid = min(BM, pend - pbeg);
