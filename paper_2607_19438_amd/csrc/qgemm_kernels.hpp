@@ -11,6 +11,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <type_traits>
 #include <stdint.h>
 
 namespace qg {
@@ -187,6 +188,15 @@ struct TileKernel {
 
 typedef __attribute__((address_space(3))) char lds_char;
 
+// LDS stages of a tile, each its own __shared__ array: the activation DMA of one stage and the
+// LDS reads / dequantised-weight writes of the others then have distinct underlying objects, so
+// the compiler can tell they do not alias and keeps the DMA in flight across them instead of
+// draining it (vmcnt) before every LDS access.
+struct LdsStages {
+  char* x[3];
+  char* w[2];
+};
+
 constexpr uint32_t kBufferFlags = 0x00020000;   // raw buffer, 32-bit dwords (gfx9 family)
 constexpr uint32_t kOOB = 0xFFFFFFF0u;          // offset past every buffer: loads return 0
 
@@ -215,19 +225,24 @@ template <int FMT, int BM, int BN, int WM, int WN, bool MOE, bool FULL, int XS, 
 __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __restrict__ wq,
                                           const uint16_t* __restrict__ sc, int m0, int n0,
                                           int rows_valid, const int* __restrict__ s_xrow,
-                                          const int* __restrict__ s_yrow, char* __restrict__ lds_generic,
+                                          const int* __restrict__ s_yrow, LdsStages st,
                                           int ks0, int nsteps, float* __restrict__ yout) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, MOE, XS>;
   static_assert(!SWI || MOE, "the fused SwiGLU epilogue is a MoE gate/up epilogue");
   constexpr int kUnitsPerChunk = (FMT == kQ8) ? 2 : 4;        // 16-byte LDS writes per 16-byte load
   constexpr int kUnits = KT::kWChunks * kUnitsPerChunk;        // per thread per K step
+  constexpr int kWD = (FMT == kQ4) ? 3 : 2;                    // weight prefetch distance (K steps)
+  // the K loop is unrolled over a period in which activation stage, weight register set and
+  // weight LDS stage (two) all repeat
+  constexpr int kPeriod = (XS == 3 || kWD == 3) ? 6 : 2;
   static_assert(kUnits % 4 == 0, "units must spread evenly over the four K16 sub-steps");
   constexpr int kUnitsPerKK = kUnits / 4;
   constexpr int kMfmaPerKK = KT::kTM * KT::kTN;
   constexpr int kValuPerUnit = (FMT == kQ8) ? 20 : 22;
   constexpr int kValuPerMfma = (kUnitsPerKK * kValuPerUnit + 4 + kMfmaPerKK - 1) / kMfmaPerKK;
 
-  lds_char* lds = (lds_char*)lds_generic;
+  auto xstage_ptr = [&](int stage) { return (lds_char*)(stage == 0 ? st.x[0] : stage == 1 ? st.x[1] : st.x[2]); };
+  auto wstage_ptr = [&](int stage) { return (lds_char*)(stage == 0 ? st.w[0] : st.w[1]); };
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -300,29 +315,35 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     for (int u = 0; u < kUnitsPerChunk; ++u) lds_w[i][u] = lds_chunk(r, c * kUnitsPerChunk + u);
   }
 
+  // Loads of steps past this tile's last one (kt_local >= nk) are issued with out-of-range
+  // offsets: the buffer range check answers them with zeros, no memory is read, and the K loop
+  // stays free of branches around its loads.
   auto issue_x = [&](int kt_local, int stage) {
     const int kt = ks0 + kt_local;
     const uint32_t kbyte = (uint32_t)kt * (uint32_t)kRowBytes;
-    const bool tail = (kt + 1) * kBK > K;
+    const bool tail = (kt + 1) * kBK > K || kt_local >= nk;
 #pragma unroll
     for (int j = 0; j < KT::kXLoads; ++j) {
       uint32_t off = (xoff[j] == kOOB) ? kOOB : xoff[j] + kbyte;
-      if (tail && (kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
-      lds_char* dst = lds + stage * KT::kXTileBytes + (wave * KT::kXLoads + j) * 1024;
+      if (tail && (kt_local >= nk || kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
+      lds_char* dst = xstage_ptr(stage) + (wave * KT::kXLoads + j) * 1024;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
     }
   };
 
-  uint4 wv[2][KT::kWChunks];
-  uint32_t sv[2][KT::kWChunks];
+  // weight register sets: the loads of step k are issued kWD steps ahead, into set k % kWD
+  uint4 wv[kWD][KT::kWChunks];
+  uint32_t sv[kWD][KT::kWChunks];
 
   auto issue_w = [&](int kt_local, uint4 (&w)[KT::kWChunks], uint32_t (&s)[KT::kWChunks]) {
     const int kt = ks0 + kt_local;
+    const bool live = kt_local < nk;
 #pragma unroll
     for (int i = 0; i < KT::kWChunks; ++i) {
-      w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                                           wr, woff[i] + (uint32_t)kt * KT::kWStepBytes, 0, 0));
-      s[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(sr, soff[i] + (uint32_t)kt * 4u, 0, 0);
+      const uint32_t wo = live ? woff[i] + (uint32_t)kt * KT::kWStepBytes : kOOB;
+      const uint32_t so = live ? soff[i] + (uint32_t)kt * 4u : kOOB;
+      w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wr, wo, 0, 0));
+      s[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(sr, so, 0, 0);
     }
   };
 
@@ -346,7 +367,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       o = dequant_q8_unit(d[2 * sub], d[2 * sub + 1], scl[i]);
     else
       o = dequant_q4_unit(d[sub], scl[i], scl16[i], soffv[i]);
-    *reinterpret_cast<lds_u32x4*>(lds + KT::kWBase + stage * KT::kWTileBytes + lds_w[i][sub]) = o;
+    *reinterpret_cast<lds_u32x4*>(wstage_ptr(stage) + lds_w[i][sub]) = o;
   };
 
   f32x16 acc[KT::kTM][KT::kTN];
@@ -376,8 +397,8 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   // the barrier that closes the K step, overlapping the next step's first LDS reads.
   bf16x8 av[2][KT::kTM], bv[2][KT::kTN];
   auto load_frags = [&](int xstage, int wstage, int kk, int buf) {
-    const lds_char* xs = lds + xstage * KT::kXTileBytes;
-    const lds_char* ws = lds + KT::kWBase + wstage * KT::kWTileBytes;
+    const lds_char* xs = xstage_ptr(xstage);
+    const lds_char* ws = wstage_ptr(wstage);
     const int slot = ((kk * 2 + lh) ^ rsw) << 4;
 #pragma unroll
     for (int j = 0; j < KT::kTN; ++j)
@@ -437,64 +458,84 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     if constexpr (FULL) __builtin_amdgcn_sched_barrier(0);
   };
 
-  // prologue: steps 0 .. XS-2 of the activations and steps 0, 1 of the weights in flight;
+  // prologue: steps 0 .. XS-2 of the activations and steps 0 .. kWD-1 of the weights in flight;
   // step 0's weights dequantised into weight stage 0
   constexpr int kAhead = XS - 1;                              // activation prefetch distance (steps)
-  constexpr int kPerStep = KT::kXLoads + 2 * KT::kWChunks;    // memory ops issued per K step
   // vmcnt retires in issue order, so waiting for a weight register set also waits for every
   // load issued before it: with three activation stages the weights of a step are issued
   // before its activations, so dequantising them never forces the younger activations.
+  // The order of the loads in flight is pinned with scheduling barriers: the waits below count
+  // the loads issued after a given activation step, which is only exact if the compiler keeps
+  // every group of loads where it is written. Weight loads of steps beyond the last one read
+  // inside the buffer range or are cut off by it (zeros), so they are issued unconditionally.
   issue_x(0, 0);
-  issue_w(0, wv[0], sv[0]);
-  if (nk > 1) issue_w(1, wv[1], sv[1]);
-  if (XS == 3 && nk > 1) issue_x(1, 1);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int k = 0; k < kWD; ++k) issue_w(k, wv[k], sv[k]);
+  __builtin_amdgcn_sched_barrier(0);
+  if (XS == 3) issue_x(1, 1);
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int u = 0; u < kUnits; ++u) dequant_unit(0, u, wv[0], sv[0], 0);
   // step 0's activations landed: allow what was issued after them to stay in flight
-  if (nk > 1) {
-    if constexpr (XS == 3) wait_vmcnt_lgkm0<kPerStep>(); else wait_vmcnt_lgkm0<2 * KT::kWChunks>();
-  } else {
-    wait_vmcnt_lgkm0<0>();
-  }
+  if (XS == 3) wait_vmcnt_lgkm0<kWD * 2 * KT::kWChunks + KT::kXLoads>();
+  else wait_vmcnt_lgkm0<kWD * 2 * KT::kWChunks>();
   __builtin_amdgcn_s_barrier();
   load_frags(0, 0, 0, 0);
 
-  // Step kt: issue activations of step kt+kAhead and weights of step kt+2, MFMA over
-  // activation stage kt % XS / weight stage kt & 1, then wait for step kt+1's activations.
-  // With two activation stages only one step of activations is in flight at the barrier
-  // (vmcnt counts the weight loads issued after it); with three, one more step's loads are.
-  auto xstage = [&](int k) { return XS == 2 ? (k & 1) : (k % 3); };
-  auto wait_next = [&](int k) {
-    if constexpr (XS == 3) {
-      if (k + 2 < nk) wait_vmcnt_lgkm0<kPerStep>(); else wait_vmcnt_lgkm0<0>();
-    } else {
-      if (k + 2 < nk) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
-    }
+  // Step kt (S = kt % kPeriod): issue the activations of step kt + kAhead and the weights of
+  // step kt + kWD, MFMA over activation stage kt % XS / weight stage kt & 1 while step kt+1's
+  // weights (register set (kt+1) % kWD) are dequantised into weight stage (kt+1) & 1, then wait
+  // for step kt+1's activations and close the step with a barrier.
+  auto step = [&](auto S_, int kt) {
+    constexpr int S = decltype(S_)::value;
+    constexpr int xs_cur = S % XS, xs_next = (S + 1) % XS, xs_ahead = (S + kAhead) % XS;
+    constexpr int wset_issue = S % kWD, wset_next = (S + 1) % kWD;
+    if (XS == 2) issue_x(kt + kAhead, xs_ahead);
+    __builtin_amdgcn_sched_barrier(0);
+    issue_w(kt + kWD, wv[wset_issue], sv[wset_issue]);
+    __builtin_amdgcn_sched_barrier(0);
+    if (XS == 3) issue_x(kt + kAhead, xs_ahead);
+    __builtin_amdgcn_sched_barrier(0);
+    step_head(kt, xs_cur, S & 1, wv[wset_next], sv[wset_next]);
+    // loads issued after x(kt+1): XS == 2 -> this step's weights; XS == 3 -> this step's
+    // weights and activations (x(kt+1) was issued one step earlier)
+    if constexpr (XS == 3) wait_vmcnt_lgkm0<2 * KT::kWChunks + KT::kXLoads>();
+    else wait_vmcnt_lgkm0<2 * KT::kWChunks>();
+    __builtin_amdgcn_s_barrier();
+    step_tail(kt + 1 < nk, xs_next, (S + 1) & 1);
   };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using I4 = std::integral_constant<int, 4>;
+  using I5 = std::integral_constant<int, 5>;
   int kt = 0;
-  for (; kt + 1 < nk; kt += 2) {
-    // even step: weights of step kt+1 are in set 1; prefetch step kt+2's weights into set 0
-    if (XS == 2 && kt + kAhead < nk) issue_x(kt + kAhead, xstage(kt + kAhead));
-    if (kt + 2 < nk) issue_w(kt + 2, wv[0], sv[0]);
-    if (XS == 3 && kt + kAhead < nk) issue_x(kt + kAhead, xstage(kt + kAhead));
-    step_head(kt, xstage(kt), 0, wv[1], sv[1]);
-    wait_next(kt);
-    __builtin_amdgcn_s_barrier();
-    step_tail(true, xstage(kt + 1), 1);
-    // odd step: weights of step kt+2 are in set 0; prefetch step kt+3's weights into set 1
-    if (XS == 2 && kt + 1 + kAhead < nk) issue_x(kt + 1 + kAhead, xstage(kt + 1 + kAhead));
-    if (kt + 3 < nk) issue_w(kt + 3, wv[1], sv[1]);
-    if (XS == 3 && kt + 1 + kAhead < nk) issue_x(kt + 1 + kAhead, xstage(kt + 1 + kAhead));
-    step_head(kt + 1, xstage(kt + 1), 1, wv[0], sv[0]);
-    wait_next(kt + 1);
-    __builtin_amdgcn_s_barrier();
-    step_tail(kt + 2 < nk, xstage(kt + 2), 0);
+  if constexpr (kPeriod == 2) {
+    for (; kt + 2 <= nk; kt += 2) {
+      step(I0{}, kt);
+      step(I1{}, kt + 1);
+    }
+    if (kt < nk) step(I0{}, kt);
+  } else {
+    for (; kt + 6 <= nk; kt += 6) {
+      step(I0{}, kt);
+      step(I1{}, kt + 1);
+      step(I2{}, kt + 2);
+      step(I3{}, kt + 3);
+      step(I4{}, kt + 4);
+      step(I5{}, kt + 5);
+    }
+    if (kt < nk) step(I0{}, kt);
+    if (kt + 1 < nk) step(I1{}, kt + 1);
+    if (kt + 2 < nk) step(I2{}, kt + 2);
+    if (kt + 3 < nk) step(I3{}, kt + 3);
+    if (kt + 4 < nk) step(I4{}, kt + 4);
   }
-  if (kt < nk) {   // odd number of steps: the last one (weight stage 0) has nothing left to fetch
-    step_head(kt, xstage(kt), 0, wv[1], sv[1]);
-    wait_vmcnt_lgkm0<0>();
-    step_tail(false, 0, 0);
-  }
+  // only out-of-range loads (past the last step) can still be in flight: retire them before the
+  // workgroup can end
+  wait_vmcnt_lgkm0<0>();
 
   // --- epilogue: lane holds column (lane & 31) and rows (r/4)*8 + (lane/32)*4 + r%4 of each block ---
   if constexpr (SWI) {
@@ -556,7 +597,7 @@ template <int FMT, int BM, int BN, int WM, int WN, bool MOE, int XS, bool SWI>
 __device__ __forceinline__ void tile_dispatch(const TileArgs& a, const uint8_t* __restrict__ wq,
                                               const uint16_t* __restrict__ sc, int m0, int n0, int rows_valid,
                                               const int* __restrict__ s_xrow, const int* __restrict__ s_yrow,
-                                              char* __restrict__ lds, int ks0, int nsteps, float* __restrict__ yout) {
+                                              LdsStages lds, int ks0, int nsteps, float* __restrict__ yout) {
   if (rows_valid == BM)
     tile_body<FMT, BM, BN, WM, WN, MOE, true, XS, SWI>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0, nsteps,
                                                        yout);
@@ -569,7 +610,12 @@ template <int FMT, int BM, int BN, int WM, int WN, int XS>
 __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const uint8_t* __restrict__ wq,
                                                              const uint16_t* __restrict__ sc) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, false, XS>;
-  __shared__ __attribute__((aligned(1024))) char lds[KT::kLdsBytes];
+  __shared__ __attribute__((aligned(1024))) char lx0[KT::kXTileBytes];
+  __shared__ __attribute__((aligned(1024))) char lx1[KT::kXTileBytes];
+  __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 16];
+  __shared__ __attribute__((aligned(1024))) char lw0[KT::kWTileBytes];
+  __shared__ __attribute__((aligned(1024))) char lw1[KT::kWTileBytes];
+  const LdsStages lds{{lx0, lx1, XS == 3 ? lx2 : nullptr}, {lw0, lw1}};
   const int mt_n = (a.M + BM - 1) / BM;
   const int nt_n = (a.N + BN - 1) / BN;
   const int ntiles = mt_n * nt_n;
@@ -597,7 +643,12 @@ template <int FMT, int BM, int BN, int WM, int WN, int XS, bool SWI>
 __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtrs ep) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, true, XS>;
   static_assert(KT::kThreads >= kMaxExpertsPerLaunch, "the tile prefix needs one lane per expert");
-  __shared__ __attribute__((aligned(1024))) char lds[KT::kLdsBytes];
+  __shared__ __attribute__((aligned(1024))) char lx0[KT::kXTileBytes];
+  __shared__ __attribute__((aligned(1024))) char lx1[KT::kXTileBytes];
+  __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 16];
+  __shared__ __attribute__((aligned(1024))) char lw0[KT::kWTileBytes];
+  __shared__ __attribute__((aligned(1024))) char lw1[KT::kWTileBytes];
+  const LdsStages lds{{lx0, lx1, XS == 3 ? lx2 : nullptr}, {lw0, lw1}};
   __shared__ int s_prefix[kMaxExpertsPerLaunch + 1];
   __shared__ int s_rowidx[BM];   // y row (assignment) of each tile row
   __shared__ int s_xrow[BM];     // x row (token = assignment / topk) of each tile row
