@@ -21,7 +21,7 @@ ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}",
     "-O3",
-    "-std=c++17",
+    "-std=c++20",
     "-fPIC",
     "-shared",
     # no packed-fp32 VALU instructions in any device code

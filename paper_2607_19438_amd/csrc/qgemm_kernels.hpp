@@ -234,12 +234,11 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   constexpr int kWD = (FMT == kQ4) ? 3 : 2;                    // weight prefetch distance (K steps)
   // the K loop is unrolled over a period in which activation stage, weight register set and
   // weight LDS stage (two) all repeat
-  constexpr int kPeriod = (XS == 3 || kWD == 3) ? 6 : 2;
+  constexpr int kPeriod = (XS == 3 || kWD == 3) ? 6 : (kWD == 4 ? 4 : 2);
   static_assert(kUnits % 4 == 0, "units must spread evenly over the four K16 sub-steps");
   constexpr int kUnitsPerKK = kUnits / 4;
   constexpr int kMfmaPerKK = KT::kTM * KT::kTN;
   constexpr int kValuPerUnit = (FMT == kQ8) ? 20 : 22;
-  constexpr int kValuPerMfma = (kUnitsPerKK * kValuPerUnit + 4 + kMfmaPerKK - 1) / kMfmaPerKK;
 
   auto xstage_ptr = [&](int stage) { return (lds_char*)(stage == 0 ? st.x[0] : stage == 1 ? st.x[1] : st.x[2]); };
   auto wstage_ptr = [&](int stage) { return (lds_char*)(stage == 0 ? st.w[0] : st.w[1]); };
@@ -324,6 +323,10 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     const bool tail = (kt + 1) * kBK > K || kt_local >= nk;
 #pragma unroll
     for (int j = 0; j < KT::kXLoads; ++j) {
+      // an 8-row group wholly past the valid rows is not fetched at all: its LDS rows keep
+      // stale data, which only reaches accumulator rows that are never stored. (With three
+      // stages the waits count this step's activation loads, so every group is issued.)
+      if (!FULL && XS == 2 && (wave * KT::kXLoads + j) * 8 >= rows_valid) continue;
       uint32_t off = (xoff[j] == kOOB) ? kOOB : xoff[j] + kbyte;
       if (tail && (kt_local >= nk || kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
       lds_char* dst = xstage_ptr(stage) + (wave * KT::kXLoads + j) * 1024;
@@ -505,34 +508,14 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     __builtin_amdgcn_s_barrier();
     step_tail(kt + 1 < nk, xs_next, (S + 1) & 1);
   };
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
-  using I4 = std::integral_constant<int, 4>;
-  using I5 = std::integral_constant<int, 5>;
   int kt = 0;
-  if constexpr (kPeriod == 2) {
-    for (; kt + 2 <= nk; kt += 2) {
-      step(I0{}, kt);
-      step(I1{}, kt + 1);
-    }
-    if (kt < nk) step(I0{}, kt);
-  } else {
-    for (; kt + 6 <= nk; kt += 6) {
-      step(I0{}, kt);
-      step(I1{}, kt + 1);
-      step(I2{}, kt + 2);
-      step(I3{}, kt + 3);
-      step(I4{}, kt + 4);
-      step(I5{}, kt + 5);
-    }
-    if (kt < nk) step(I0{}, kt);
-    if (kt + 1 < nk) step(I1{}, kt + 1);
-    if (kt + 2 < nk) step(I2{}, kt + 2);
-    if (kt + 3 < nk) step(I3{}, kt + 3);
-    if (kt + 4 < nk) step(I4{}, kt + 4);
-  }
+  // whole periods, then the remaining steps (each guarded by the step count)
+  auto period = [&]<int... S>(std::integer_sequence<int, S...>) {
+    for (; kt + kPeriod <= nk; kt += kPeriod) (step(std::integral_constant<int, S>{}, kt + S), ...);
+    ((kt + S < nk && S < kPeriod - 1 ? (step(std::integral_constant<int, S>{}, kt + S), 0) : 0), ...);
+  };
+  period(std::make_integer_sequence<int, kPeriod>{});
+
   // only out-of-range loads (past the last step) can still be in flight: retire them before the
   // workgroup can end
   wait_vmcnt_lgkm0<0>();
