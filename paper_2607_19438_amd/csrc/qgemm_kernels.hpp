@@ -481,8 +481,16 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
 #pragma unroll
   for (int u = 0; u < kUnits; ++u) dequant_unit(0, u, wv[0], sv[0], 0);
   // step 0's activations landed: allow what was issued after them to stay in flight
-  if (XS == 3) wait_vmcnt_lgkm0<kWD * 2 * KT::kWChunks + KT::kXLoads>();
-  else wait_vmcnt_lgkm0<kWD * 2 * KT::kWChunks>();
+  // Weight loads whose registers are never read again (steps past the last one, j > nk) may be
+  // deleted by the compiler, so a wait counts only the weight loads that are certainly issued
+  // (j <= nk): an undercount only makes the wait stricter.
+  {
+    const int w_live = min(kWD, nk + 1);
+    constexpr int kX1 = XS == 3 ? KT::kXLoads : 0;
+    if (w_live >= 3) wait_vmcnt_lgkm0<3 * 2 * KT::kWChunks + kX1>();
+    else if (w_live == 2) wait_vmcnt_lgkm0<2 * 2 * KT::kWChunks + kX1>();
+    else wait_vmcnt_lgkm0<2 * KT::kWChunks + kX1>();
+  }
   __builtin_amdgcn_s_barrier();
   load_frags(0, 0, 0, 0);
 
@@ -503,8 +511,13 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     step_head(kt, xs_cur, S & 1, wv[wset_next], sv[wset_next]);
     // loads issued after x(kt+1): XS == 2 -> this step's weights; XS == 3 -> this step's
     // weights and activations (x(kt+1) was issued one step earlier)
-    if constexpr (XS == 3) wait_vmcnt_lgkm0<2 * KT::kWChunks + KT::kXLoads>();
-    else wait_vmcnt_lgkm0<2 * KT::kWChunks>();
+    // (weight loads of steps past the last one may be deleted: counted only when live)
+    const bool w_live = kt + kWD <= nk;
+    if constexpr (XS == 3) {
+      if (w_live) wait_vmcnt_lgkm0<2 * KT::kWChunks + KT::kXLoads>(); else wait_vmcnt_lgkm0<KT::kXLoads>();
+    } else {
+      if (w_live) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
+    }
     __builtin_amdgcn_s_barrier();
     step_tail(kt + 1 < nk, xs_next, (S + 1) & 1);
   };

@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import check_levels, dev_w, dev_x, report, sample_pairs, torch_or_skip
+from gpu_util import check_levels, dev_w, dev_x, report, sample_pairs, tight_ratio, torch_or_skip
 
 pytestmark = pytest.mark.gpu
 
@@ -67,10 +67,14 @@ RAGGED = [
     (1000, 700, 4096 + 32),  # split-K over 5, K tail inside the last split
     (512, 512, 8192),      # split-K over 4 (the down-projection shape class)
 ]
+# every K-step count modulo the unrolled loop period (2 or 6 steps) and each K tail position,
+# on the 128x128 tile (M < 256) and the 256x256 tile
+K_STEPS = [(255, 257, 64 * s + t) for s, t in ((3, 32), (4, 0), (4, 32), (5, 0), (6, 32), (7, 0), (9, 32), (11, 0), (13, 32))]
+K_STEPS += [(3584, 3840, K) for K in (288, 448, 736)]       # 210 tiles of 256x256, no split
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-@pytest.mark.parametrize("M,N,K", RAGGED)
+@pytest.mark.parametrize("M,N,K", RAGGED + K_STEPS)
 def test_ragged_shapes(fmt, M, N, K):
     torch = torch_or_skip()
     case = synth.dense_case(f"ragged_{synth.FMT_NAMES[fmt]}_{M}x{N}x{K}", fmt, M, N, K, seed=5, stream=(M, N, K))
@@ -141,3 +145,19 @@ def test_unit_scale_q_one_gives_row_sums_on_gpu():
         babs = np.abs(oracle.decode_bf16(x)).sum(axis=1)
         # unit weights are exact in bf16: only fp32 summation error remains
         assert np.all(np.abs(y - rs[:, None]) <= oracle.fp32_sum_rel(K) * babs[:, None])
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_every_k_step_count_repeated(fmt):
+    """One 128x128 tile for K = 64 .. 832 (1 to 13 K steps, with and without a half step), each
+    run four times: the prefetch pipeline's waits must hold on every repetition, in every
+    position of the unrolled loop period."""
+    torch = torch_or_skip()
+    for steps in range(1, 14):
+        for K in (64 * steps, 64 * steps - 32):
+            case = synth.dense_case(f"repeat_{synth.FMT_NAMES[fmt]}_K{K}", fmt, 128, 128, K, seed=9, stream=(K,))
+            ref = oracle.dense(case.x, case.w.wq, case.w.scales, fmt, bf16_weights=True)
+            for _ in range(4):
+                y = run_dense(torch, case)
+                assert tight_ratio(y, ref[0], ref[1], K) <= 1.0, f"K={K}"
+
