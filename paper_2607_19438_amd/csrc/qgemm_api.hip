@@ -186,7 +186,7 @@ int grow(int32_t** p, size_t* cap, size_t need) {
 }
 
 int bucket_geometry(int n, int* chunk, int* nblk) {
-  int c = 4096;
+  int c = 512;   // one or two rounds of the scatter per block, and >= 100 blocks at 64K slots
   long nb = ((long)n + c - 1) / c;
   if (nb > 1024) {
     c = (int)((((long)n + 1023) / 1024 + 255) / 256 * 256);
@@ -441,12 +441,21 @@ int qgemm_moe_combine(const float* y2, const float* route_w, float* out, int T, 
   if (!y2 || !route_w || !out) return fail(QGEMM_EINVAL, "null pointer argument");
   if (!aligned16(y2) || !aligned16(out) || !aligned16(route_w))
     return fail(QGEMM_EALIGN, "y2, route_w and out must be 16-byte aligned");
-  const long groups = (long)T * (N / 4);
+  const int v = (N % 8 == 0) ? 8 : 4;
+  const long groups = (long)T * (N / v);
   const long blocks = (groups + 255) / 256;
   if (blocks > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "problem too large");
   (void)hipGetLastError();
-  hipLaunchKernelGGL(qg::combine_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, y2, route_w, out, groups,
-                     topk, N);
+  // top-8 routing (the paper's MoE models) gets a kernel with every slot's loads issued up front
+  if (v == 8 && topk == 8)
+    hipLaunchKernelGGL((qg::combine_kernel<8, 8>), dim3((unsigned)blocks), dim3(256), 0, stream, y2, route_w, out,
+                       groups, topk, N);
+  else if (v == 8)
+    hipLaunchKernelGGL((qg::combine_kernel<8, 0>), dim3((unsigned)blocks), dim3(256), 0, stream, y2, route_w, out,
+                       groups, topk, N);
+  else
+    hipLaunchKernelGGL((qg::combine_kernel<4, 0>), dim3((unsigned)blocks), dim3(256), 0, stream, y2, route_w, out,
+                       groups, topk, N);
   const int rc = check_launch("qgemm_moe_combine");
   return rc == QGEMM_OK ? ok() : rc;
 }

@@ -52,6 +52,7 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_scatter_kernel(
     const int hi = offsets[e + 1];
     long c = lo;
     long tot = 0;
+#pragma unroll 16
     for (int b = 0; b < nblk; ++b) {
       const int v = counts[(long)b * E + e];
       if (b < (int)blockIdx.x) c += v;
@@ -136,24 +137,58 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ y
 }
 
 // out[t][n] = sum_j w[t*topk+j] * y2[t*topk+j][n], fp32 fused multiply-add in increasing j.
+// Each thread produces V (4 or 8) consecutive outputs of one token row, keeping V/4 * topk
+// independent 16-byte loads in flight; y2 is read exactly once, so its loads and the output
+// stores are non-temporal.
+template <int V, int KFIX>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ y2, const float* __restrict__ w,
-                                                      float* __restrict__ out, long groups, int topk, int N) {
+                                                      float* __restrict__ out, long groups, int topk_rt, int N) {
+  static_assert(V == 4 || V == 8, "4 or 8 outputs per thread");
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  constexpr int G = V / 4;
+  const int topk = KFIX > 0 ? KFIX : topk_rt;
   const long gid = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= groups) return;
-  const int per_row = N >> 2;
+  const int per_row = N / V;
   const long t = gid / per_row;
-  const int n0 = (int)(gid - t * per_row) * 4;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int j = 0; j < topk; ++j) {
-    const long a = t * topk + j;
-    const float wj = w[a];
-    const float4 v = *reinterpret_cast<const float4*>(y2 + a * N + n0);
-    acc.x = __builtin_fmaf(wj, v.x, acc.x);
-    acc.y = __builtin_fmaf(wj, v.y, acc.y);
-    acc.z = __builtin_fmaf(wj, v.z, acc.z);
-    acc.w = __builtin_fmaf(wj, v.w, acc.w);
+  const int n0 = (int)(gid - t * per_row) * V;
+  f32x4 acc[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (KFIX > 0) {
+    // every slot's loads first, then the FMAs in slot order
+    f32x4 v[KFIX][G];
+    float wj[KFIX];
+#pragma unroll
+    for (int j = 0; j < KFIX; ++j) {
+      const long a = t * KFIX + j;
+      wj[j] = w[a];
+      const f32x4* src = reinterpret_cast<const f32x4*>(y2 + a * N + n0);
+#pragma unroll
+      for (int g = 0; g < G; ++g) v[j][g] = __builtin_nontemporal_load(src + g);
+    }
+#pragma unroll
+    for (int j = 0; j < KFIX; ++j)
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[g][c] = __builtin_fmaf(wj[j], v[j][g][c], acc[g][c]);
+  } else {
+    for (int j = 0; j < topk; ++j) {
+      const long a = t * topk + j;
+      const float wj = w[a];
+      const f32x4* src = reinterpret_cast<const f32x4*>(y2 + a * N + n0);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const f32x4 v = __builtin_nontemporal_load(src + g);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[g][c] = __builtin_fmaf(wj, v[c], acc[g][c]);
+      }
+    }
   }
-  *reinterpret_cast<float4*>(out + t * N + n0) = acc;
+  f32x4* dst = reinterpret_cast<f32x4*>(out + t * N + n0);
+#pragma unroll
+  for (int g = 0; g < G; ++g) __builtin_nontemporal_store(acc[g], dst + g);
 }
 
 // y[i] = sum_{s < splits} ws[s][i], summed in increasing s (deterministic); 4 floats per thread.

@@ -138,11 +138,20 @@ def test_swiglu_and_combine_small():
     hv = oracle.decode_bf16(hb)
     # bf16 output: within one bf16 ulp-ish of the fp64 value (2^-7 relative) plus tiny absolute slack
     assert np.all(np.abs(hv - href) <= 2.0 ** -7 * np.abs(href) + 1e-30)
-    y2 = rng.standard_normal((rows, N)).astype(np.float32)
-    w = rng.uniform(0.01, 1.0, rows).astype(np.float32)
-    out = q().moe_combine(dev_f32(torch, y2), dev_f32(torch, w), topk).cpu().numpy()
-    oref, bnd = oracle.combine(y2.astype(np.float64), w, topk, np.abs(y2).astype(np.float64))
-    assert oracle.within_bar(out, oref, bnd).all()
+    # the three combine kernels: 8 outputs per thread with top-8 fixed, 8 with any top-k, 4 (N % 8 != 0)
+    for topk_c, N_c in ((topk, N), (8, 48), (8, 52), (3, 44)):
+        rows_c = 24 * topk_c
+        y2 = rng.standard_normal((rows_c, N_c)).astype(np.float32)
+        w = rng.uniform(0.01, 1.0, rows_c).astype(np.float32)
+        out = q().moe_combine(dev_f32(torch, y2), dev_f32(torch, w), topk_c).cpu().numpy()
+        oref, bnd = oracle.combine(y2.astype(np.float64), w, topk_c, np.abs(y2).astype(np.float64))
+        assert oracle.within_bar(out, oref, bnd).all(), (topk_c, N_c)
+        # fp32 FMA in increasing slot order: reproduce it exactly on the host
+        exp = np.zeros((rows_c // topk_c, N_c), np.float32)
+        for j in range(topk_c):
+            exp = (w[j::topk_c, None].astype(np.float64) * y2[j::topk_c].astype(np.float64)
+                   + exp.astype(np.float64)).astype(np.float32)
+        assert np.array_equal(out, exp), (topk_c, N_c)
 
 
 def moe_ffn_gpu(torch, case, split=False):
