@@ -120,6 +120,13 @@ __device__ __forceinline__ void wait_vmcnt_lgkm0() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
 }
 
+// s_waitcnt lgkmcnt(0) only (vector memory loads stay in flight)
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
+
+#ifndef QG_PINGPONG
+#define QG_PINGPONG 1
+#endif
+
 // ---------------------------------------------------------------------------
 // tile kernel
 // ---------------------------------------------------------------------------
@@ -209,6 +216,9 @@ constexpr int kSchedMFMA = 0x008;
 constexpr int kSchedVALU = 0x002;
 constexpr int kSchedDSRead = 0x100;
 constexpr int kSchedDSWrite = 0x200;
+#ifndef QG_K_AFTER
+#define QG_K_AFTER 1
+#endif
 
 // One output tile: rows [m0, m0 + rows_valid) of x (dense) or the gathered rows
 // s_xrow[] (MoE), columns [n0, n0 + BN) of W.
@@ -240,6 +250,22 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   constexpr int kMfmaPerKK = KT::kTM * KT::kTN;
   constexpr int kValuPerUnit = (FMT == kQ8) ? 20 : 22;
 
+  // Ping-pong (8-wave tiles): the two waves sharing a SIMD belong to different wave rows (wm).
+  // Per K step, wm = 1 waves issue the activation DMA while wm = 0 waves run their MFMAs; after
+  // a barrier, wm = 1 waves run their MFMAs while wm = 0 waves load and dequantise the next
+  // step's weights; a second barrier closes the step. One wave per SIMD issues MFMAs at a time,
+  // with its partner's memory and VALU work in the other issue slots, instead of both waves
+  // arriving at one barrier at different times.
+  constexpr bool PP = QG_PINGPONG && WM == 2 && WN == 4 && XS == 2;
+  constexpr int XL = PP ? 2 * KT::kXLoads : KT::kXLoads;        // DMA loads per DMA-role wave
+  // Weight chunks per thread: without ping-pong every thread takes kWChunks. With it the wm = 0
+  // waves take CQ chunks (dequantised after their MFMA phase) and the wm = 1 waves CD chunks
+  // (dequantised in their DMA phase), so the two phases carry similar non-MFMA work.
+  constexpr int CQ = PP ? (KT::kWChunks >= 2 ? (3 * KT::kWChunks + 1) / 2 : KT::kWChunks) : KT::kWChunks;
+  constexpr int CD = PP ? 2 * KT::kWChunks - CQ : KT::kWChunks;
+  constexpr int WC = CQ > CD ? CQ : CD;                           // register arrays sized for either role
+  static_assert(!PP || CQ + CD == 2 * KT::kWChunks, "every chunk dequantised once");
+  constexpr int kWStride = PP ? KT::kThreads / 2 : KT::kThreads;
   auto xstage_ptr = [&](int stage) { return (lds_char*)(stage == 0 ? st.x[0] : stage == 1 ? st.x[1] : st.x[2]); };
   auto wstage_ptr = [&](int stage) { return (lds_char*)(stage == 0 ? st.w[0] : st.w[1]); };
   const int tid = threadIdx.x;
@@ -253,29 +279,35 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   const uint32_t kblocks = (uint32_t)K >> 5;
   const uint32_t wrow_bytes = (FMT == kQ8) ? (uint32_t)K : (uint32_t)K >> 1;
   const int n_valid = min(BN, N - n0);
+  const bool isD = PP ? wm == 1 : true;            // issues activation DMA
+  const bool isQ = PP ? wm == 0 : true;            // loads and dequantises weights
+  const int xw = PP ? (isD ? wave - WN : 0) : wave;  // DMA wave index within its role
+  // first weight chunk of this thread: dequant threads t take chunks t + i * stride (i < CQ), DMA
+  // threads t' take CQ * stride + t' + i * stride (i < CD)
+  const int wt = PP ? (isQ ? tid : CQ * (KT::kThreads / 2) + (tid - KT::kThreads / 2)) : tid;
 
   // --- activation DMA: this lane fetches logical chunk dma_c[j] of row (8 g + lane / 8) ---
   __amdgpu_buffer_rsrc_t xr;
-  uint32_t xoff[KT::kXLoads];
-  int dma_c[KT::kXLoads];
+  uint32_t xoff[XL];
+  int dma_c[XL];
 #pragma unroll
-  for (int j = 0; j < KT::kXLoads; ++j) {
-    const int r = (wave * KT::kXLoads + j) * 8 + (lane >> 3);
+  for (int j = 0; j < XL; ++j) {
+    const int r = (xw * XL + j) * 8 + (lane >> 3);
     dma_c[j] = (lane & 7) ^ ((r >> 1) & 7);     // the chunk that lds_chunk(r, .) places at slot lane & 7
   }
   if constexpr (MOE) {
     xr = make_rsrc(a.x, (uint32_t)a.T * (uint32_t)K * 2u);
 #pragma unroll
-    for (int j = 0; j < KT::kXLoads; ++j) {
-      const int r = (wave * KT::kXLoads + j) * 8 + (lane >> 3);
+    for (int j = 0; j < XL; ++j) {
+      const int r = (xw * XL + j) * 8 + (lane >> 3);
       const int src = (r < rows_valid) ? s_xrow[r] : -1;
       xoff[j] = (src >= 0) ? (uint32_t)src * (uint32_t)K * 2u + (uint32_t)dma_c[j] * 16u : kOOB;
     }
   } else {
     xr = make_rsrc(a.x + (size_t)m0 * K, (uint32_t)rows_valid * (uint32_t)K * 2u);
 #pragma unroll
-    for (int j = 0; j < KT::kXLoads; ++j) {
-      const int r = (wave * KT::kXLoads + j) * 8 + (lane >> 3);
+    for (int j = 0; j < XL; ++j) {
+      const int r = (xw * XL + j) * 8 + (lane >> 3);
       xoff[j] = (uint32_t)r * (uint32_t)K * 2u + (uint32_t)dma_c[j] * 16u;
     }
   }
@@ -290,14 +322,14 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       SWI ? make_rsrc(wq, (uint32_t)N * wrow_bytes) : make_rsrc(wq + (size_t)n0 * wrow_bytes, (uint32_t)n_valid * wrow_bytes);
   const __amdgpu_buffer_rsrc_t sr = SWI ? make_rsrc(sc, (uint32_t)N * kblocks * 2u)
                                         : make_rsrc(sc + (size_t)n0 * kblocks, (uint32_t)n_valid * kblocks * 2u);
-  uint32_t woff[KT::kWChunks];
-  uint32_t soff[KT::kWChunks];
-  int lds_w[KT::kWChunks][kUnitsPerChunk];   // LDS byte offset (within the W tile) of each unit
-  int wcol[KT::kWChunks];
-  bool wrow_ok[KT::kWChunks];
+  uint32_t woff[WC];
+  uint32_t soff[WC];
+  int lds_w[WC][kUnitsPerChunk];   // LDS byte offset (within the W tile) of each unit
+  int wcol[WC];
+  bool wrow_ok[WC];
 #pragma unroll
-  for (int i = 0; i < KT::kWChunks; ++i) {
-    const int q = tid + i * KT::kThreads;
+  for (int i = 0; i < WC; ++i) {
+    const int q = wt + i * kWStride;
     const int r = q / KT::kWChunksPerRow;
     const int c = q % KT::kWChunksPerRow;
     int grow = r;
@@ -322,27 +354,28 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     const uint32_t kbyte = (uint32_t)kt * (uint32_t)kRowBytes;
     const bool tail = (kt + 1) * kBK > K || kt_local >= nk;
 #pragma unroll
-    for (int j = 0; j < KT::kXLoads; ++j) {
+    for (int j = 0; j < XL; ++j) {
       // an 8-row group wholly past the valid rows is not fetched at all: its LDS rows keep
       // stale data, which only reaches accumulator rows that are never stored. (With three
       // stages the waits count this step's activation loads, so every group is issued.)
-      if (!FULL && XS == 2 && (wave * KT::kXLoads + j) * 8 >= rows_valid) continue;
+      if (!FULL && XS == 2 && (xw * XL + j) * 8 >= rows_valid) continue;
       uint32_t off = (xoff[j] == kOOB) ? kOOB : xoff[j] + kbyte;
       if (tail && (kt_local >= nk || kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
-      lds_char* dst = xstage_ptr(stage) + (wave * KT::kXLoads + j) * 1024;
+      lds_char* dst = xstage_ptr(stage) + (xw * XL + j) * 1024;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
     }
   };
 
   // weight register sets: the loads of step k are issued kWD steps ahead, into set k % kWD
-  uint4 wv[kWD][KT::kWChunks];
-  uint32_t sv[kWD][KT::kWChunks];
+  uint4 wv[kWD][WC];
+  uint32_t sv[kWD][WC];
 
-  auto issue_w = [&](int kt_local, uint4 (&w)[KT::kWChunks], uint32_t (&s)[KT::kWChunks]) {
+  auto issue_w = [&](int kt_local, uint4 (&w)[WC], uint32_t (&s)[WC], int cnt) {
     const int kt = ks0 + kt_local;
     const bool live = kt_local < nk;
 #pragma unroll
-    for (int i = 0; i < KT::kWChunks; ++i) {
+    for (int i = 0; i < WC; ++i) {
+      if (i >= cnt) break;
       const uint32_t wo = live ? woff[i] + (uint32_t)kt * KT::kWStepBytes : kOOB;
       const uint32_t so = live ? soff[i] + (uint32_t)kt * 4u : kOOB;
       w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wr, wo, 0, 0));
@@ -351,9 +384,8 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   };
 
   // dequantise unit u (0 <= u < kUnits) of a weight register set into LDS stage `stage`
-  float scl[KT::kWChunks], scl16[KT::kWChunks], soffv[KT::kWChunks];
-  auto dequant_unit = [&](int kt, int u, const uint4 (&w)[KT::kWChunks], const uint32_t (&s)[KT::kWChunks],
-                          int stage) {
+  float scl[WC], scl16[WC], soffv[WC];
+  auto dequant_unit = [&](int kt, int u, const uint4 (&w)[WC], const uint32_t (&s)[WC], int stage) {
     const int i = u / kUnitsPerChunk;
     const int sub = u % kUnitsPerChunk;
     if (sub == 0) {
@@ -420,17 +452,21 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       }
     }
   };
-  // dequantisation units of the next step, spread over sub-steps 0..2 (they must land before the barrier)
-  constexpr int kUnitGroups = 3;
+  // The MFMAs of the last kAfter sub-steps of a step run after the barrier that closes it, so a
+  // wave that reaches the barrier early still has that much matrix work queued behind it.
+  constexpr int kAfter = QG_K_AFTER;
+  constexpr int kHead = 4 - kAfter;                  // sub-steps whose MFMAs run before the barrier
+  // dequantisation units of the next step, spread over the head sub-steps (they must land before
+  // the barrier)
+  constexpr int kUnitGroups = kHead;
   auto unit_lo = [](int kk) { return (kk * kUnits + kUnitGroups - 1) / kUnitGroups; };
 
-  // sub-steps 0..2 of step kt over activation stage xcur and weight stage wcur (fragments of
-  // sub-step 0 already in set 0), with step kt+1's weights (set wn_) dequantised into weight
-  // stage wcur ^ 1; leaves sub-step 3's fragments in set 1
-  auto step_head = [&](int kt, int xcur, int wcur, const uint4 (&wn_)[KT::kWChunks],
-                       const uint32_t (&sn_)[KT::kWChunks]) {
+  // head of step kt over activation stage xcur and weight stage wcur (fragments of sub-step 0
+  // already in set 0), with step kt+1's weights (set wn_) dequantised into weight stage wcur ^ 1;
+  // leaves the fragments of the last kAfter sub-steps in their sets (sub-step kk in set kk & 1)
+  auto step_head = [&](int kt, int xcur, int wcur, const uint4 (&wn_)[WC], const uint32_t (&sn_)[WC]) {
 #pragma unroll
-    for (int kk = 0; kk < 3; ++kk) {
+    for (int kk = 0; kk < kHead; ++kk) {
       const int buf = kk & 1;
       load_frags(xcur, wcur, kk + 1, buf ^ 1);
       mfmas(buf);
@@ -453,82 +489,185 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+    // with two sub-steps after the barrier, sub-step 3's fragments load into the set that
+    // sub-step 1's MFMAs (just issued) read
+    if constexpr (kAfter == 2) {
+      load_frags(xcur, wcur, 3, 1);
+      if constexpr (FULL) __builtin_amdgcn_sched_barrier(0);
+    }
   };
-  // after the barrier: next step's sub-step 0 fragments (if any) while sub-step 3's MFMAs run
+  // after the barrier: the last kAfter sub-steps' MFMAs, with the next step's sub-step 0
+  // fragments (if any) loaded into set 0 once the MFMAs reading set 0 have issued
   auto step_tail = [&](bool next, int next_xstage, int next_wstage) {
-    if (next) load_frags(next_xstage, next_wstage, 0, 0);
-    mfmas(1);
+    if constexpr (kAfter == 2) {
+      mfmas(0);
+      if constexpr (FULL) __builtin_amdgcn_sched_barrier(0);
+      if (next) load_frags(next_xstage, next_wstage, 0, 0);
+      mfmas(1);
+    } else {
+      if (next) load_frags(next_xstage, next_wstage, 0, 0);
+      mfmas(1);
+    }
     if constexpr (FULL) __builtin_amdgcn_sched_barrier(0);
   };
 
-  // prologue: steps 0 .. XS-2 of the activations and steps 0 .. kWD-1 of the weights in flight;
-  // step 0's weights dequantised into weight stage 0
-  constexpr int kAhead = XS - 1;                              // activation prefetch distance (steps)
-  // vmcnt retires in issue order, so waiting for a weight register set also waits for every
-  // load issued before it: with three activation stages the weights of a step are issued
-  // before its activations, so dequantising them never forces the younger activations.
-  // The order of the loads in flight is pinned with scheduling barriers: the waits below count
-  // the loads issued after a given activation step, which is only exact if the compiler keeps
-  // every group of loads where it is written. Weight loads of steps beyond the last one read
-  // inside the buffer range or are cut off by it (zeros), so they are issued unconditionally.
-  issue_x(0, 0);
-  __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-  for (int k = 0; k < kWD; ++k) issue_w(k, wv[k], sv[k]);
-  __builtin_amdgcn_sched_barrier(0);
-  if (XS == 3) issue_x(1, 1);
-  __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-  for (int u = 0; u < kUnits; ++u) dequant_unit(0, u, wv[0], sv[0], 0);
-  // step 0's activations landed: allow what was issued after them to stay in flight
-  // Weight loads whose registers are never read again (steps past the last one, j > nk) may be
-  // deleted by the compiler, so a wait counts only the weight loads that are certainly issued
-  // (j <= nk): an undercount only makes the wait stricter.
-  {
-    const int w_live = min(kWD, nk + 1);
-    constexpr int kX1 = XS == 3 ? KT::kXLoads : 0;
-    if (w_live >= 3) wait_vmcnt_lgkm0<3 * 2 * KT::kWChunks + kX1>();
-    else if (w_live == 2) wait_vmcnt_lgkm0<2 * 2 * KT::kWChunks + kX1>();
-    else wait_vmcnt_lgkm0<2 * KT::kWChunks + kX1>();
-  }
-  __builtin_amdgcn_s_barrier();
-  load_frags(0, 0, 0, 0);
-
-  // Step kt (S = kt % kPeriod): issue the activations of step kt + kAhead and the weights of
-  // step kt + kWD, MFMA over activation stage kt % XS / weight stage kt & 1 while step kt+1's
-  // weights (register set (kt+1) % kWD) are dequantised into weight stage (kt+1) & 1, then wait
-  // for step kt+1's activations and close the step with a barrier.
-  auto step = [&](auto S_, int kt) {
-    constexpr int S = decltype(S_)::value;
-    constexpr int xs_cur = S % XS, xs_next = (S + 1) % XS, xs_ahead = (S + kAhead) % XS;
-    constexpr int wset_issue = S % kWD, wset_next = (S + 1) % kWD;
-    if (XS == 2) issue_x(kt + kAhead, xs_ahead);
+  if constexpr (!PP) {
+    // prologue: steps 0 .. XS-2 of the activations and steps 0 .. kWD-1 of the weights in flight;
+    // step 0's weights dequantised into weight stage 0
+    constexpr int kAhead = XS - 1;                              // activation prefetch distance (steps)
+    // vmcnt retires in issue order, so waiting for a weight register set also waits for every
+    // load issued before it: with three activation stages the weights of a step are issued
+    // before its activations, so dequantising them never forces the younger activations.
+    // The order of the loads in flight is pinned with scheduling barriers: the waits below count
+    // the loads issued after a given activation step, which is only exact if the compiler keeps
+    // every group of loads where it is written. Weight loads of steps beyond the last one read
+    // inside the buffer range or are cut off by it (zeros), so they are issued unconditionally.
+    issue_x(0, 0);
     __builtin_amdgcn_sched_barrier(0);
-    issue_w(kt + kWD, wv[wset_issue], sv[wset_issue]);
+  #pragma unroll
+    for (int k = 0; k < kWD; ++k) issue_w(k, wv[k], sv[k], WC);
     __builtin_amdgcn_sched_barrier(0);
-    if (XS == 3) issue_x(kt + kAhead, xs_ahead);
+    if (XS == 3) issue_x(1, 1);
     __builtin_amdgcn_sched_barrier(0);
-    step_head(kt, xs_cur, S & 1, wv[wset_next], sv[wset_next]);
-    // loads issued after x(kt+1): XS == 2 -> this step's weights; XS == 3 -> this step's
-    // weights and activations (x(kt+1) was issued one step earlier)
-    // (weight loads of steps past the last one may be deleted: counted only when live)
-    const bool w_live = kt + kWD <= nk;
-    if constexpr (XS == 3) {
-      if (w_live) wait_vmcnt_lgkm0<2 * KT::kWChunks + KT::kXLoads>(); else wait_vmcnt_lgkm0<KT::kXLoads>();
-    } else {
-      if (w_live) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
+  #pragma unroll
+    for (int u = 0; u < kUnits; ++u) dequant_unit(0, u, wv[0], sv[0], 0);
+    // step 0's activations landed: allow what was issued after them to stay in flight
+    // Weight loads whose registers are never read again (steps past the last one, j > nk) may be
+    // deleted by the compiler, so a wait counts only the weight loads that are certainly issued
+    // (j <= nk): an undercount only makes the wait stricter.
+    {
+      const int w_live = min(kWD, nk + 1);
+      constexpr int kX1 = XS == 3 ? KT::kXLoads : 0;
+      if (w_live >= 3) wait_vmcnt_lgkm0<3 * 2 * KT::kWChunks + kX1>();
+      else if (w_live == 2) wait_vmcnt_lgkm0<2 * 2 * KT::kWChunks + kX1>();
+      else wait_vmcnt_lgkm0<2 * KT::kWChunks + kX1>();
     }
     __builtin_amdgcn_s_barrier();
-    step_tail(kt + 1 < nk, xs_next, (S + 1) & 1);
-  };
-  int kt = 0;
-  // whole periods, then the remaining steps (each guarded by the step count)
-  auto period = [&]<int... S>(std::integer_sequence<int, S...>) {
-    for (; kt + kPeriod <= nk; kt += kPeriod) (step(std::integral_constant<int, S>{}, kt + S), ...);
-    ((kt + S < nk && S < kPeriod - 1 ? (step(std::integral_constant<int, S>{}, kt + S), 0) : 0), ...);
-  };
-  period(std::make_integer_sequence<int, kPeriod>{});
+    load_frags(0, 0, 0, 0);
 
+    // Step kt (S = kt % kPeriod): issue the activations of step kt + kAhead and the weights of
+    // step kt + kWD, MFMA over activation stage kt % XS / weight stage kt & 1 while step kt+1's
+    // weights (register set (kt+1) % kWD) are dequantised into weight stage (kt+1) & 1, then wait
+    // for step kt+1's activations and close the step with a barrier.
+    auto step = [&](auto S_, int kt) {
+      constexpr int S = decltype(S_)::value;
+      constexpr int xs_cur = S % XS, xs_next = (S + 1) % XS, xs_ahead = (S + kAhead) % XS;
+      constexpr int wset_issue = S % kWD, wset_next = (S + 1) % kWD;
+      if (XS == 2) issue_x(kt + kAhead, xs_ahead);
+      __builtin_amdgcn_sched_barrier(0);
+      issue_w(kt + kWD, wv[wset_issue], sv[wset_issue], WC);
+      __builtin_amdgcn_sched_barrier(0);
+      if (XS == 3) issue_x(kt + kAhead, xs_ahead);
+      __builtin_amdgcn_sched_barrier(0);
+      step_head(kt, xs_cur, S & 1, wv[wset_next], sv[wset_next]);
+      // loads issued after x(kt+1): XS == 2 -> this step's weights; XS == 3 -> this step's
+      // weights and activations (x(kt+1) was issued one step earlier)
+      // (weight loads of steps past the last one may be deleted: counted only when live)
+      const bool w_live = kt + kWD <= nk;
+      if constexpr (XS == 3) {
+        if (w_live) wait_vmcnt_lgkm0<2 * KT::kWChunks + KT::kXLoads>(); else wait_vmcnt_lgkm0<KT::kXLoads>();
+      } else {
+        if (w_live) wait_vmcnt_lgkm0<2 * KT::kWChunks>(); else wait_vmcnt_lgkm0<0>();
+      }
+      __builtin_amdgcn_s_barrier();
+      step_tail(kt + 1 < nk, xs_next, (S + 1) & 1);
+    };
+    int kt = 0;
+    // whole periods, then the remaining steps (each guarded by the step count)
+    auto period = [&]<int... S>(std::integer_sequence<int, S...>) {
+      for (; kt + kPeriod <= nk; kt += kPeriod) (step(std::integral_constant<int, S>{}, kt + S), ...);
+      ((kt + S < nk && S < kPeriod - 1 ? (step(std::integral_constant<int, S>{}, kt + S), 0) : 0), ...);
+    };
+    period(std::make_integer_sequence<int, kPeriod>{});
+  } else {
+    // ---- ping-pong K loop (see PP above) ----
+    // One wave's MFMAs for a whole step: fragments of sub-step kk+1 load while sub-step kk's
+    // MFMAs run; sub-step 0's fragments are already in set 0 when `pre` is set.
+    auto mfma_phase = [&](int xst, int wst, bool pre) {
+      if (!pre) load_frags(xst, wst, 0, 0);
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        if (kk < 3) load_frags(xst, wst, kk + 1, (kk + 1) & 1);
+        mfmas(kk & 1);
+        if constexpr (FULL) {
+          QG_SG(kSchedMFMA, 1);
+          if (kk < 3) QG_SG(kSchedDSRead, KT::kTM + KT::kTN);
+          QG_SG(kSchedMFMA, kMfmaPerKK - 1);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    };
+    // prologue: activations of step 0 (DMA waves), weights of steps 0 .. kWD-1 in flight and
+    // step 0's dequantised into weight stage 0 (dequant waves)
+    if (isD) {
+      issue_x(0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int k = 0; k < kWD; ++k) issue_w(k, wv[k], sv[k], CD);
+#pragma unroll
+      for (int u = 0; u < CD * kUnitsPerChunk; ++u) dequant_unit(0, u, wv[0], sv[0], 0);
+      wait_vmcnt_lgkm0<0>();
+    } else {
+#pragma unroll
+      for (int k = 0; k < kWD; ++k) issue_w(k, wv[k], sv[k], CQ);
+#pragma unroll
+      for (int u = 0; u < CQ * kUnitsPerChunk; ++u) dequant_unit(0, u, wv[0], sv[0], 0);
+      // a dequant wave waits for its LDS writes only (its weight registers are waited on where
+      // they are read)
+      wait_lgkm0();
+    }
+    __builtin_amdgcn_s_barrier();
+
+    // The two roles run separate loops (the role branch taken once, outside the K loop, so the
+    // accumulators never meet at a join); both execute two barriers per step.
+    auto q_step = [&](auto S_, int kt) {
+      constexpr int S = decltype(S_)::value;
+      constexpr int xs_cur = S % 2, ws_cur = S & 1;
+      constexpr int wset_issue = S % kWD, wset_next = (S + 1) % kWD;
+      mfma_phase(xs_cur, ws_cur, false);                   // stage kt complete since the last barrier
+      __builtin_amdgcn_s_barrier();
+      issue_w(kt + kWD, wv[wset_issue], sv[wset_issue], CQ);  // the set of step kt, dequantised last step
+#pragma unroll
+      for (int u = 0; u < CQ * kUnitsPerChunk; ++u)
+        dequant_unit(kt + 1, u, wv[wset_next], sv[wset_next], ws_cur ^ 1);
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+    };
+    auto d_step = [&](auto S_, int kt) {
+      constexpr int S = decltype(S_)::value;
+      constexpr int xs_cur = S % 2, xs_next = (S + 1) % 2, ws_cur = S & 1;
+      constexpr int wset_issue = S % kWD, wset_next = (S + 1) % kWD;
+      issue_x(kt + 1, xs_next);                            // stage last read in step kt-1
+      __builtin_amdgcn_sched_barrier(0);                   // the wait below counts the loads after the DMA
+      issue_w(kt + kWD, wv[wset_issue], sv[wset_issue], CD);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < CD * kUnitsPerChunk; ++u)
+        dequant_unit(kt + 1, u, wv[wset_next], sv[wset_next], ws_cur ^ 1);
+      load_frags(xs_cur, ws_cur, 0, 0);                    // prefetch for the MFMA phase
+      __builtin_amdgcn_s_barrier();
+      mfma_phase(xs_cur, ws_cur, true);
+      // this wave's activation DMA of step kt+1: the only vector-memory loads issued after it are
+      // its weight loads of step kt+kWD, counted only when live (loads of steps past the last one
+      // may be deleted, and an undercount only makes the wait stricter)
+      if (kt + kWD <= nk) wait_vmcnt_lgkm0<2 * CD>(); else wait_vmcnt_lgkm0<0>();
+      __builtin_amdgcn_s_barrier();
+    };
+    int kt = 0;
+    if (isQ) {
+      auto period = [&]<int... S>(std::integer_sequence<int, S...>) {
+        for (; kt + kPeriod <= nk; kt += kPeriod) (q_step(std::integral_constant<int, S>{}, kt + S), ...);
+        ((kt + S < nk && S < kPeriod - 1 ? (q_step(std::integral_constant<int, S>{}, kt + S), 0) : 0), ...);
+      };
+      period(std::make_integer_sequence<int, kPeriod>{});
+    } else {
+      auto period = [&]<int... S>(std::integer_sequence<int, S...>) {
+        for (; kt + kPeriod <= nk; kt += kPeriod) (d_step(std::integral_constant<int, S>{}, kt + S), ...);
+        ((kt + S < nk && S < kPeriod - 1 ? (d_step(std::integral_constant<int, S>{}, kt + S), 0) : 0), ...);
+      };
+      period(std::make_integer_sequence<int, kPeriod>{});
+    }
+  }
   // only out-of-range loads (past the last step) can still be in flight: retire them before the
   // workgroup can end
   wait_vmcnt_lgkm0<0>();
