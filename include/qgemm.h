@@ -147,6 +147,8 @@ int qgemm_moe_gate_up_swiglu(const void* x, const int32_t* perm, const int32_t* 
  * SiLU-gated activation between the MoE projections (Section 3.1, fused
  * gate/up item): for r < rows, i < inter,
  *   h[r][i] = bf16_rne(silu(y1[r][i]) * y1[r][inter + i]),  silu(z) = z / (1 + e^-z)
+ * evaluated in fp32 with the hardware exponential and reciprocal (about one
+ * fp32 ulp each, below the bf16 rounding of h).
  * y1: fp32 [rows][2*inter]; h: bf16 [rows][inter]. inter % 8 == 0.
  */
 int qgemm_swiglu(const float* y1, void* h, int rows, int inter, hipStream_t stream);

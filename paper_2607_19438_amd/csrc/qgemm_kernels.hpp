@@ -83,7 +83,11 @@ __device__ __forceinline__ void dequant_q4x32(const uint4 w, float s, uint32_t o
 
 // h = silu(g) * u in fp32 (the SiLU-gated activation); shared by the fused epilogue and the
 // standalone kernel so both round the same fp32 value to bf16.
-__device__ __forceinline__ float swiglu_f32(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
+// silu(g) = g / (1 + e^-g) with the hardware exponential and reciprocal (each within about one
+// fp32 ulp, far below the bf16 rounding of h); g -> -inf gives 1 / inf = 0, so silu -> -0.
+__device__ __forceinline__ float swiglu_f32(float g, float u) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+}
 
 // One 16-byte LDS unit of dequantised weights = 8 bf16.
 // Q8: two dwords of int8 (8 weights) with scale s.
