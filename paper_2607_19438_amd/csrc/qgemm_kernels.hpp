@@ -19,6 +19,7 @@ namespace qg {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
@@ -710,6 +711,46 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     return;
   }
   const bool full_cols = n0 + BN <= N;
+  if (full_cols && (N & 3) == 0) {
+    // Row-contiguous stores through LDS: each 32x32 accumulator block goes to a per-wave LDS
+    // scratch (row stride 40 floats: the two row halves a store instruction writes fall in
+    // disjoint banks) and comes back as 16-byte row chunks, so a wave stores a block with 4
+    // dwordx4 instructions instead of 16 dword ones. Every wave is past its last LDS read of the
+    // K loop (the loop ends with a barrier after the last fragment reads and DMA waits).
+    constexpr int kStride = 40;
+    constexpr int kHalf = KT::kWaves / 2;
+    static_assert(kHalf * 32 * kStride * 4 <= KT::kXTileBytes, "epilogue scratch must fit an activation stage");
+    lds_char* scratch = xstage_ptr(wave / kHalf) + (wave % kHalf) * (32 * kStride * 4);
+    const int rr = lane >> 3;                 // row within an 8-row read group
+    const int cc = (lane & 7) * 4;            // first of this lane's 4 columns
+#pragma unroll
+    for (int i = 0; i < KT::kTM; ++i) {
+      if (!FULL && i >= mblocks) continue;
+      const int rbase = (i * WM + wm) * 32;
+#pragma unroll
+      for (int j = 0; j < KT::kTN; ++j) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = (r >> 2) * 8 + lh * 4 + (r & 3);
+          *reinterpret_cast<__attribute__((address_space(3))) float*>(scratch + (row * kStride + lr) * 4) =
+              acc[i][j][r];
+        }
+        const int col = n0 + wn * KT::kWTN + j * 32 + cc;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int row = g * 8 + rr;
+          const f32x4 v =
+              *reinterpret_cast<const __attribute__((address_space(3))) f32x4*>(scratch + (row * kStride + cc) * 4);
+          const int trow = rbase + row;
+          if (!FULL && trow >= rows_valid) continue;
+          const int dst = MOE ? s_yrow[trow] : (m0 + trow);
+          if (MOE && dst < 0) continue;
+          *reinterpret_cast<f32x4*>(yout + (size_t)dst * N + col) = v;
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < KT::kTM; ++i) {
     if (!FULL && i >= mblocks) continue;
