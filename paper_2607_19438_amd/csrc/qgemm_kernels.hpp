@@ -684,6 +684,53 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     // (0 <= q < 8) and receives their up values, the odd lane keeps rows q + 8 and receives their
     // gate values, so every lane evaluates the SiLU gate for 8 rows and stores them.
     const bool odd = (lr & 1) != 0;
+    // Staged path: a wave's h columns (h0 + wn * kWTN / 2 + [0, kWTN / 2)) all valid and rows
+    // 16-byte aligned: h values go through a per-wave LDS scratch and leave as 16-byte row chunks
+    // (8 bf16); the K loop ends with a barrier after its last LDS access.
+    constexpr int kHW = KT::kWTN / 2;             // h columns per wave
+    static_assert(kHW % 8 == 0, "whole 16-byte chunks per wave row");
+    if ((swi_inter & 7) == 0 && h0 + (wn + 1) * kHW <= swi_inter) {
+      constexpr int kStrideH = kHW + 8;           // bf16 per scratch row (16-byte aligned rows)
+      constexpr int kHalf = KT::kWaves / 2;
+      static_assert(kHalf * 32 * kStrideH * 2 <= KT::kXTileBytes, "epilogue scratch must fit an activation stage");
+      lds_char* scratch = xstage_ptr(wave / kHalf) + (wave % kHalf) * (32 * kStrideH * 2);
+      constexpr int kChunksRow = kHW / 8;
+#pragma unroll
+      for (int i = 0; i < KT::kTM; ++i) {
+        if (!FULL && i >= mblocks) continue;
+#pragma unroll
+        for (int j = 0; j < KT::kTN; ++j) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float lo = acc[i][j][q];
+            const float hi = acc[i][j][q + 8];
+            const float recv = __builtin_bit_cast(
+                float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, odd ? lo : hi), 0xB1, 0xF, 0xF, false));
+            const float g = odd ? recv : lo;
+            const float u = odd ? hi : recv;
+            const int rm = odd ? q + 8 : q;
+            const int row = (rm >> 2) * 8 + lh * 4 + (rm & 3);
+            const int hcol = j * 16 + (lr >> 1);
+            *reinterpret_cast<__attribute__((address_space(3))) uint16_t*>(scratch + (row * kStrideH + hcol) * 2) =
+                (uint16_t)(pack_bf16x2(swiglu_f32(g, u), 0.0f) & 0xFFFFu);
+          }
+        }
+        const int rbase = (i * WM + wm) * 32;
+#pragma unroll
+        for (int g = 0; g < 32 * kChunksRow / 64; ++g) {
+          const int idx = g * 64 + lane;
+          const int row = idx / kChunksRow;
+          const int ch = idx % kChunksRow;
+          const u32x4 v = *reinterpret_cast<const lds_u32x4*>(scratch + (row * kStrideH + ch * 8) * 2);
+          const int trow = rbase + row;
+          if (!FULL && trow >= rows_valid) continue;
+          const int dst = s_yrow[trow];
+          if (dst < 0) continue;
+          *reinterpret_cast<u32x4*>(a.h + (size_t)dst * swi_inter + h0 + wn * kHW + ch * 8) = v;
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < KT::kTM; ++i) {
       if (!FULL && i >= mblocks) continue;
