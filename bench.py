@@ -53,6 +53,10 @@ def parse():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (for scaling HBM byte counters) and exit")
     ap.add_argument("--only", default="", help="comma list of parts to run: dense_gate_up,dense_down,moe_t2048,moe_t8192")
+    ap.add_argument("--small-m-launches", type=int, default=200,
+                    help="launches per small-M (decode / verification) case; 0 skips that section")
+    ap.add_argument("--small-m-only", action="store_true",
+                    help="run only the small-M section and print its JSON (for kernel traces of those cases)")
     return ap.parse_args()
 
 
@@ -170,6 +174,66 @@ class EventTimer:
         return {k: float(np.mean(v)) for k, v in out.items()}
 
 
+# Small-M (decode / speculative verification) cases: the prefill projection shapes at M <= 16
+# rows, where the call is bound by HBM bandwidth. Reported beside the step, not part of `value`.
+SMALL_M_SHAPES = (("dense_q8_gate_up", 0, 8192, 2048), ("dense_q8_down", 0, 2048, 8192), ("dense_q4", 1, 8192, 3072))
+SMALL_M_ROWS = (1, 4, 16)
+ROTATE_BYTES = 1 << 30     # weight copies cycled per shape: four times the 256 MiB last-level cache
+
+
+def small_m_section(torch, q, synth, launches):
+    """Per-launch time of the small-M path with the weights read from HBM (copies rotated)."""
+    dev = torch.device("cuda:0")
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    # calibrate the device-side sleep used to keep the GPU busy while launches are enqueued
+    a, b = ev(), ev()
+    a.record()
+    torch.cuda._sleep(1 << 22)
+    b.record()
+    torch.cuda.synchronize()
+    ms_per_cycle = a.elapsed_time(b) / (1 << 22)
+    rows = []
+    for name, fmt, N, K in SMALL_M_SHAPES:
+        case = synth.dense_case("small_m_" + name, fmt, max(SMALL_M_ROWS), N, K, seed=12, stream=(N, K))
+        wq0 = torch.from_numpy(case.w.wq).to(dev)
+        sc0 = torch.from_numpy(case.w.scales).to(dev)
+        wbytes = wq0.numel() + 2 * sc0.numel()
+        R = max(2, -(-ROTATE_BYTES // wbytes))
+        copies = [(wq0.clone(), sc0.clone()) for _ in range(R)]
+        x_all = torch.from_numpy(np.ascontiguousarray(case.x).view(np.int16)).view(torch.bfloat16).to(dev)
+        for M in SMALL_M_ROWS:
+            x = x_all[:M].contiguous()
+            y = torch.empty((M, N), dtype=torch.float32, device=dev)
+            for wq, sc in copies:
+                q.dense(x, wq, sc, fmt, out=y)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(20):
+                q.dense(x, *copies[i % R], fmt, out=y)
+            host_us = (time.perf_counter() - t0) / 20 * 1e6
+            torch.cuda.synchronize()
+            # launches back to back between two events; a device-side sleep in front keeps the GPU
+            # busy until the host has enqueued them all, so host overhead does not enter the time
+            first, last = ev(), ev()
+            torch.cuda._sleep(int(3 * launches * host_us * 1e-3 / ms_per_cycle))
+            first.record()
+            for i in range(launches):
+                q.dense(x, *copies[i % R], fmt, out=y)
+            last.record()
+            torch.cuda.synchronize()
+            us = first.elapsed_time(last) / launches * 1e3
+            nbytes = wbytes + 2 * M * K + 4 * M * N
+            rows.append({"shape": name, "fmt": "q8" if fmt == 0 else "q4", "M": M, "N": N, "K": K,
+                         "bytes_per_launch": nbytes, "us_per_launch": us,
+                         "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_hbm": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS})
+            log(f"small-M {name} M={M}: {us:.2f} us/launch back to back ({rows[-1]['GB/s']:.0f} GB/s), "
+                f"{R} weight copies, host enqueue {host_us:.1f} us")
+        del copies, wq0, sc0
+        torch.cuda.empty_cache()
+    return {"bound": "hbm", "peak": PEAK_HBM_GBS, "unit": "GB/s", "weights_rotated_bytes": ROTATE_BYTES,
+            "cases": rows}
+
+
 def measured_traffic(part):
     """HBM bytes per launch from the committed counter summary, if the kernel sources are unchanged."""
     import hashlib
@@ -254,6 +318,9 @@ def main():
     import paper_2607_19438_amd as q
     import synth
     q.lib()
+    if args.small_m_only:
+        print(json.dumps({"small_m": small_m_section(torch, q, synth, args.small_m_launches)}), flush=True)
+        return 0
     log("generating inputs")
     t0 = time.perf_counter()
     parts = build_parts(torch, q, synth, args.only, fused=not args.unfused)
@@ -307,6 +374,11 @@ def main():
                 "launch_ms": per[dom], "flop_per_launch": flops_of[dom]}
     log(f"instrumented pass: {wall_ev / args.steps * 1e3:.3f} ms/step")
 
+    small = None
+    if args.small_m_launches > 0 and not args.only:
+        log("small-M (decode / verification) cases")
+        small = small_m_section(torch, q, synth, args.small_m_launches)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
@@ -324,6 +396,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "breakdown": breakdown,
+        "small_m": small,
     }
     print(json.dumps(line), flush=True)
     return 0

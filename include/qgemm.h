@@ -70,6 +70,12 @@ enum qgemm_status {
  * workgroups and sums their fp32 partials in split order (deterministic) in a
  * library-owned workspace (grown on first use, freed by qgemm_release);
  * concurrent calls on different streams must not share it.
+ * M <= 16 (decode and speculative-draft verification, the memory-bound
+ * regime of Section 4.1 and the batched verification of Section 6) takes a
+ * separate bandwidth-oriented kernel: weights dequantised straight into
+ * matrix-core registers, K split over waves (and over workgroups when N is
+ * small, through the same workspace); its results are bitwise reproducible
+ * but not bitwise equal to the M > 16 kernels (another summation order).
  */
 int qgemm_dense(const void* x, const void* wq, const void* scales, float* y,
                 int M, int N, int K, int fmt, hipStream_t stream);

@@ -14,6 +14,7 @@
 #include "../../include/qgemm.h"
 #include "qgemm_kernels.hpp"
 #include "qgemm_aux.hpp"
+#include "qgemm_smallm.hpp"
 
 namespace {
 
@@ -89,8 +90,67 @@ int split_workspace(size_t floats, float** out) {
 
 constexpr int kMinStepsPerSplit = 12;
 
+constexpr long kSmTargetGroups = 256;   // workgroups (of eight waves) to fill the CUs without a K split
+constexpr int kSmMaxJW = 8;             // chunks per wave held in registers
+
+template <int FMT, int JW>
+int launch_small(const qg::SmallArgs& a, long groups, hipStream_t s) {
+  hipLaunchKernelGGL((qg::smallm_kernel<FMT, JW, qg::kSmWaves>), dim3((unsigned)groups), dim3(qg::kSmWaves * 64),
+                     qg::smallm_scale_lds_bytes(a.nbp_log2), s, a);
+  return check_launch("qgemm_dense (small M)");
+}
+
+// M <= 16: 32 weight rows per workgroup; K is split over workgroups only when there are fewer
+// than kSmTargetGroups row blocks (or a wave would hold more than kSmMaxJW chunks). Split
+// partials go to the split-K workspace and a second kernel adds them in split order.
+template <int FMT>
+int small_dispatch(const qg::TileArgs& t, const void* wq, const void* sc, hipStream_t s) {
+  using F = qg::SmallFmt<FMT>;
+  const long nc = (t.K + F::kKC - 1) / F::kKC;
+  const long P = (t.N + qg::kSmRows - 1) / qg::kSmRows;
+  long S = std::min<long>(nc, (kSmTargetGroups + P - 1) / P);
+  S = std::max<long>(S, (nc + qg::kSmWaves * kSmMaxJW - 1) / (qg::kSmWaves * kSmMaxJW));
+  const long cps = (nc + S - 1) / S;
+  S = (nc + cps - 1) / cps;
+  if (P * S > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "too many workgroups");
+  int JW = 1;
+  while (JW * qg::kSmWaves < cps) JW *= 2;
+  int nbp_log2 = 0;
+  while ((1L << nbp_log2) < cps * F::kBPC) ++nbp_log2;
+  qg::SmallArgs a{};
+  a.x = t.x;
+  a.wq = static_cast<const uint8_t*>(wq);
+  a.sc = static_cast<const uint16_t*>(sc);
+  a.y = t.y;
+  a.M = t.M;
+  a.N = t.N;
+  a.K = t.K;
+  a.splits = (int)S;
+  a.cps = (int)cps;
+  a.nbp_log2 = nbp_log2;
+  std::unique_lock<std::mutex> lock(g_split_mutex, std::defer_lock);
+  const long total = (long)t.M * t.N;
+  if (S > 1) {
+    lock.lock();
+    int rc = split_workspace((size_t)S * total, &a.ws);
+    if (rc != QGEMM_OK) return rc;
+  }
+  int rc;
+  switch (JW) {
+    case 1: rc = launch_small<FMT, 1>(a, P * S, s); break;
+    case 2: rc = launch_small<FMT, 2>(a, P * S, s); break;
+    case 4: rc = launch_small<FMT, 4>(a, P * S, s); break;
+    default: rc = launch_small<FMT, 8>(a, P * S, s); break;
+  }
+  if (rc != QGEMM_OK || S == 1) return rc;
+  hipLaunchKernelGGL(qg::smallm_reduce_kernel, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, s, a.ws, a.y,
+                     total, (int)S);
+  return check_launch("qgemm_dense (small M) split reduction");
+}
+
 template <int FMT>
 int dense_dispatch(qg::TileArgs a, const void* wq, const void* sc, hipStream_t s) {
+  if (a.M <= qg::kSmMaxM) return small_dispatch<FMT>(a, wq, sc, s);
   a.splits = 1;
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
   if (a.M >= 256 && a.N >= 256 && big >= 200) return launch_dense<FMT, 256, 256, 2, 4, 2>(a, wq, sc, s);
