@@ -284,3 +284,46 @@ def config(i: int, seed: int = 0, T_override: int | None = None):
         T = T_override or 8192
         return [moe_case(f"moe_q4_skewed_t{T}_e128_top8", FMT_Q4, T, 128, 8, 2048, 768, 1.2, seed, (4, T))]
     raise ValueError(f"no config {i}")
+
+
+# ---------------------------------------------------------------------------
+# prefill attention inputs
+# ---------------------------------------------------------------------------
+
+@dataclass
+class AttnCase:
+    name: str
+    B: int
+    S: int
+    H: int
+    Hkv: int
+    D: int
+    causal: bool
+    scale: float
+    q: np.ndarray    # bf16 bits [B][S][H][D]
+    k: np.ndarray    # bf16 bits [B][S][Hkv][D]
+    v: np.ndarray    # bf16 bits [B][S][Hkv][D]
+
+    @property
+    def flops(self) -> float:
+        """2 products (Q K^T, P V) x 2 flops per multiply-add x D, over the visible (query, key) pairs."""
+        pairs = self.S * (self.S + 1) // 2 if self.causal else self.S * self.S
+        return 4.0 * self.B * self.H * self.D * pairs
+
+
+def attn_case(name: str, B: int, S: int, H: int, Hkv: int, D: int, causal: bool = True, seed: int = 0,
+              stream=(5,), q_std: float = 1.0) -> AttnCase:
+    """q, k, v ~ N(0, 1) (q scaled by q_std, which sharpens the softmax), bf16; scale 1/sqrt(D)."""
+    q = bf16_bits(rng_for(seed, *stream, 0).standard_normal((B, S, H, D)) * q_std)
+    k = bf16_bits(rng_for(seed, *stream, 1).standard_normal((B, S, Hkv, D)))
+    v = bf16_bits(rng_for(seed, *stream, 2).standard_normal((B, S, Hkv, D)))
+    return AttnCase(name, B, S, H, Hkv, D, causal, 1.0 / float(np.sqrt(D)), q, k, v)
+
+
+# The attention layer of the MoE workload's model family (hidden 2048, 128 experts, top-8):
+# 32 query heads and 4 key/value heads of dimension 128, a 2048-token prompt, causal.
+ATTN_PREFILL = dict(B=1, S=2048, H=32, Hkv=4, D=128, causal=True)
+
+
+def attn_prefill_case(seed: int = 0) -> AttnCase:
+    return attn_case("attn_prefill_2048", seed=seed, stream=(6,), **ATTN_PREFILL)
