@@ -55,6 +55,10 @@ def parse():
     ap.add_argument("--only", default="", help="comma list of parts to run: dense_gate_up,dense_down,moe_t2048,moe_t8192")
     ap.add_argument("--small-m-launches", type=int, default=200,
                     help="launches per small-M (decode / verification) case; 0 skips that section")
+    ap.add_argument("--attention-launches", type=int, default=50,
+                    help="launches of the prefill-attention case; 0 skips that section")
+    ap.add_argument("--attention-only", action="store_true",
+                    help="run only the prefill-attention section and print its JSON")
     ap.add_argument("--small-m-only", action="store_true",
                     help="run only the small-M section and print its JSON (for kernel traces of those cases)")
     return ap.parse_args()
@@ -234,6 +238,31 @@ def small_m_section(torch, q, synth, launches):
             "cases": rows}
 
 
+def attention_section(torch, q, synth, launches):
+    """Prefill attention of the MoE model family's layer (S=2048, 32/4 heads, D=128, causal)."""
+    dev = torch.device("cuda:0")
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    case = synth.attn_prefill_case()
+    t = lambda bits: torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+    qd, kd, vd = t(case.q), t(case.k), t(case.v)
+    o = torch.empty_like(qd)
+    for _ in range(10):
+        q.attention_prefill(qd, kd, vd, True, case.scale, out=o)
+    torch.cuda.synchronize()
+    first, last = ev(), ev()
+    first.record()
+    for _ in range(launches):
+        q.attention_prefill(qd, kd, vd, True, case.scale, out=o)
+    last.record()
+    torch.cuda.synchronize()
+    us = first.elapsed_time(last) / launches * 1e3
+    tflops = case.flops / (us * 1e-6) / 1e12
+    log(f"prefill attention S=2048 H=32/4 D=128 causal: {us:.1f} us/launch, {tflops:.0f} TFLOP/s")
+    return {"workload": "prefill attention B=1 S=2048 H=32 Hkv=4 D=128 causal bf16", "us_per_launch": us,
+            "flop_per_launch": case.flops, "TFLOP/s": tflops, "frac_mfma": tflops / PEAK_BF16_TFLOPS,
+            "launches": launches}
+
+
 def measured_traffic(part):
     """HBM bytes per launch from the committed counter summary, if the kernel sources are unchanged."""
     import hashlib
@@ -318,6 +347,9 @@ def main():
     import paper_2607_19438_amd as q
     import synth
     q.lib()
+    if args.attention_only:
+        print(json.dumps({"attention": attention_section(torch, q, synth, args.attention_launches)}), flush=True)
+        return 0
     if args.small_m_only:
         print(json.dumps({"small_m": small_m_section(torch, q, synth, args.small_m_launches)}), flush=True)
         return 0
@@ -379,6 +411,11 @@ def main():
         log("small-M (decode / verification) cases")
         small = small_m_section(torch, q, synth, args.small_m_launches)
 
+    attn = None
+    if args.attention_launches > 0 and not args.only:
+        log("prefill attention")
+        attn = attention_section(torch, q, synth, args.attention_launches)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
@@ -397,6 +434,7 @@ def main():
         "cpu_baseline": cpu,
         "breakdown": breakdown,
         "small_m": small,
+        "attention": attn,
     }
     print(json.dumps(line), flush=True)
     return 0

@@ -171,6 +171,25 @@ int qgemm_moe_combine(const float* y2, const float* route_w, float* out,
 /* Message of the last non-OK return on the calling thread ("" if none). */
 const char* qgemm_last_error(void);
 
+/*
+ * Prefill attention (Section 3.1, prefill attention item): softmax attention of a prompt's
+ * queries over its keys, with the score product and the output product on the matrix cores and
+ * an exact online softmax (running row maximum) between them. For every batch entry b, query
+ * head h and query position i:
+ *   s_j = scale * (q[b][i][h] . k[b][j][g]),  g = h / (H / Hkv)   (grouped-query attention)
+ *   o[b][i][h] = sum_j softmax(s)_j v[b][j][g]
+ * over the keys j <= i (causal = 1: prefill from an empty cache) or all keys j < S (causal = 0).
+ * q, o: bf16 [B][S][H][D]; k, v: bf16 [B][S][Hkv][D]; every tensor contiguous, token-major,
+ * 16-byte aligned; caller-owned device memory. D is 64 or 128; H a multiple of Hkv;
+ * S*H*D < 2^31. Accumulation is fp32; the softmax weights enter the output product as bf16
+ * and o is rounded to bf16 (nearest even). scale > 0 (1/sqrt(D) for the usual models).
+ * Returns QGEMM_EINVAL / QGEMM_EUNSUPPORTED / QGEMM_EALIGN before launching anything (o is
+ * untouched) and QGEMM_EHIP if the launch fails; B == 0 or S == 0 is a no-op.
+ */
+int qgemm_attention_prefill(const void* q, const void* k, const void* v, void* o,
+                            int B, int S, int H, int Hkv, int D,
+                            float scale, int causal, hipStream_t stream);
+
 /* Frees the library-owned workspaces (MoE bucketing, split-K partials); the
  * next call that needs one grows it again. The caller must have synchronised
  * every stream that used them. */

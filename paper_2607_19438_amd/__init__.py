@@ -16,7 +16,7 @@ import os
 import torch  # imported before the library so that both share one HIP runtime
 
 __all__ = ["Q8", "Q4", "QGemmError", "lib", "lib_path", "dense", "moe", "moe_bucket", "moe_grouped",
-           "moe_gate_up_swiglu", "swiglu", "moe_combine", "last_error", "release", "version", "EXPORTS", "ExpertTable"]
+           "moe_gate_up_swiglu", "swiglu", "moe_combine", "attention_prefill", "last_error", "release", "version", "EXPORTS", "ExpertTable"]
 
 Q8 = 0
 Q4 = 1
@@ -34,6 +34,7 @@ EXPORTS = {
     "qgemm_moe_gate_up_swiglu": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "qgemm_swiglu": (_i, [_vp, _vp, _i, _i, _vp]),
     "qgemm_moe_combine": (_i, [_vp, _vp, _vp, _i, _i, _i, _vp]),
+    "qgemm_attention_prefill": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, ctypes.c_float, _i, _vp]),
     "qgemm_last_error": (ctypes.c_char_p, []),
     "qgemm_release": (_i, []),
     "qgemm_version": (_i, []),
@@ -278,4 +279,26 @@ def moe_combine(y2, route_w, topk: int, out=None):
         out = torch.empty((T, N), dtype=torch.float32, device=y2.device)
     _need(out, "out", (torch.float32,), 2)
     _check(lib().qgemm_moe_combine(y2.data_ptr(), route_w.data_ptr(), out.data_ptr(), T, topk, N, _stream(y2)))
+    return out
+
+
+def attention_prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: bool = True,
+                      scale: float | None = None, out: torch.Tensor | None = None):
+    """``qgemm_attention_prefill``: q ``[B][S][H][D]``, k / v ``[B][S][Hkv][D]`` bf16 -> o ``[B][S][H][D]`` bf16."""
+    _need(q, "q", (torch.bfloat16,), 4)
+    _need(k, "k", (torch.bfloat16,), 4)
+    _need(v, "v", (torch.bfloat16,), 4)
+    B, S, H, D = q.shape
+    if k.shape != v.shape or k.shape[0] != B or k.shape[1] != S or k.shape[3] != D:
+        raise ValueError("q, k and v disagree on B, S or D")
+    Hkv = k.shape[2]
+    if scale is None:
+        scale = 1.0 / float(D) ** 0.5
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out, "out", (torch.bfloat16,), 4)
+    if out.shape != q.shape:
+        raise ValueError("out must have the shape of q")
+    _check(lib().qgemm_attention_prefill(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), B, S, H, Hkv, D,
+                                         float(scale), int(bool(causal)), _stream(q)))
     return out

@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libqgemm.so")
 SOURCES = [os.path.join(CSRC, "qgemm_api.hip")]
-DEPS = SOURCES + [os.path.join(CSRC, f) for f in ("qgemm_kernels.hpp", "qgemm_aux.hpp", "qgemm_smallm.hpp")] + [
+DEPS = SOURCES + [os.path.join(CSRC, f) for f in ("qgemm_kernels.hpp", "qgemm_aux.hpp", "qgemm_smallm.hpp", "attn_kernels.hpp")] + [
     os.path.join(os.path.dirname(HERE), "include", "qgemm.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

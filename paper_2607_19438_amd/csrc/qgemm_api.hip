@@ -2,6 +2,7 @@
 // contract of every entry point are in include/qgemm.h).
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -15,6 +16,7 @@
 #include "qgemm_kernels.hpp"
 #include "qgemm_aux.hpp"
 #include "qgemm_smallm.hpp"
+#include "attn_kernels.hpp"
 
 namespace {
 
@@ -517,6 +519,44 @@ int qgemm_moe_combine(const float* y2, const float* route_w, float* out, int T, 
     hipLaunchKernelGGL((qg::combine_kernel<4, 0>), dim3((unsigned)blocks), dim3(256), 0, stream, y2, route_w, out,
                        groups, topk, N);
   const int rc = check_launch("qgemm_moe_combine");
+  return rc == QGEMM_OK ? ok() : rc;
+}
+
+int qgemm_attention_prefill(const void* q, const void* k, const void* v, void* o, int B, int S, int H, int Hkv, int D,
+                            float scale, int causal, hipStream_t stream) {
+  if (B < 0 || S < 0) return fail(QGEMM_EINVAL, "B and S must be >= 0 (got %d, %d)", B, S);
+  if (H < 1 || Hkv < 1 || H % Hkv != 0)
+    return fail(QGEMM_EINVAL, "H and Hkv must be >= 1 with H a multiple of Hkv (got %d, %d)", H, Hkv);
+  if (D != 64 && D != 128) return fail(QGEMM_EUNSUPPORTED, "head dimension must be 64 or 128 (got %d)", D);
+  if (causal != 0 && causal != 1) return fail(QGEMM_EINVAL, "causal must be 0 or 1 (got %d)", causal);
+  if (!(scale > 0.0f) || !std::isfinite(scale)) return fail(QGEMM_EINVAL, "scale must be finite and > 0");
+  if ((long)S * H * D > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "S*H*D must be below 2^31");
+  const long nqb = (S + qg::kAttnBQ - 1) / qg::kAttnBQ;
+  if ((long)B * H * nqb > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "too many workgroups");
+  if (B == 0 || S == 0) return ok();
+  if (!q || !k || !v || !o) return fail(QGEMM_EINVAL, "null pointer argument");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+    return fail(QGEMM_EALIGN, "q, k, v and o must be 16-byte aligned");
+  (void)hipGetLastError();
+  qg::AttnArgs a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.o = static_cast<uint16_t*>(o);
+  a.B = B;
+  a.S = S;
+  a.H = H;
+  a.Hkv = Hkv;
+  a.sl2 = (float)((double)scale * 1.4426950408889634);   // exp(x) = exp2(x log2 e)
+  const dim3 grid((unsigned)(B * H * nqb)), block(qg::kAttnThreads);
+  if (D == 128) {
+    if (causal) hipLaunchKernelGGL((qg::attn_fwd_kernel<128, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((qg::attn_fwd_kernel<128, false>), grid, block, 0, stream, a);
+  } else {
+    if (causal) hipLaunchKernelGGL((qg::attn_fwd_kernel<64, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((qg::attn_fwd_kernel<64, false>), grid, block, 0, stream, a);
+  }
+  const int rc = check_launch("qgemm_attention_prefill");
   return rc == QGEMM_OK ? ok() : rc;
 }
 

@@ -33,7 +33,7 @@ def header_prototypes():
 def test_header_declares_the_boundary():
     p = header_prototypes()
     for name in ("qgemm_dense", "qgemm_moe", "qgemm_moe_bucket", "qgemm_moe_grouped", "qgemm_moe_gate_up_swiglu", "qgemm_swiglu",
-                 "qgemm_moe_combine", "qgemm_last_error", "qgemm_release", "qgemm_version"):
+                 "qgemm_moe_combine", "qgemm_attention_prefill", "qgemm_last_error", "qgemm_release", "qgemm_version"):
         assert name in p
 
 
@@ -93,6 +93,25 @@ def test_moe_host_validation(qmod):
     assert lib.qgemm_swiglu(16, 16, 0, 16, None) == 0
     assert lib.qgemm_moe_combine(16, 16, 16, 4, 2, 6, None) == -1
     assert lib.qgemm_moe_combine(16, 16, 16, 0, 2, 8, None) == 0
+
+
+def test_attention_host_validation(qmod):
+    lib = qmod.lib()
+    f = lib.qgemm_attention_prefill
+    # q, k, v, o, B, S, H, Hkv, D, scale, causal, stream
+    assert f(16, 16, 16, 16, 1, 8, 6, 4, 128, 0.1, 1, None) == -1    # H not a multiple of Hkv
+    assert f(16, 16, 16, 16, 1, 8, 4, 0, 128, 0.1, 1, None) == -1    # Hkv < 1
+    assert f(16, 16, 16, 16, 1, 8, 4, 4, 96, 0.1, 1, None) == -3     # unsupported head dimension
+    assert f(16, 16, 16, 16, 1, 8, 4, 4, 128, 0.1, 2, None) == -1    # causal not 0/1
+    assert f(16, 16, 16, 16, 1, 8, 4, 4, 128, 0.0, 1, None) == -1    # scale <= 0
+    assert f(16, 16, 16, 16, 1, 8, 4, 4, 128, float("nan"), 1, None) == -1
+    assert f(16, 16, 16, 16, -1, 8, 4, 4, 128, 0.1, 1, None) == -1   # B < 0
+    assert f(16, 16, 16, 16, 1, 1 << 20, 32, 4, 128, 0.1, 1, None) == -3   # S*H*D >= 2^31
+    assert f(16, 16, 16, 16, 0, 8, 4, 4, 128, 0.1, 1, None) == 0     # empty batch: no-op
+    assert f(16, 16, 16, 16, 1, 0, 4, 4, 128, 0.1, 1, None) == 0     # empty prompt: no-op
+    assert f(None, 16, 16, 16, 1, 8, 4, 4, 128, 0.1, 1, None) == -1  # null pointer
+    assert f(16, 16, 24, 16, 1, 8, 4, 4, 128, 0.1, 1, None) == -2    # v misaligned
+    assert "16-byte" in qmod.last_error()
 
 
 def test_product_never_imports_oracle():
