@@ -38,31 +38,54 @@ struct AttnArgs {
   float sl2;           // softmax scale * log2(e)
 };
 
+// The kernel body lives in a device function (the kernel below only forwards to it): its
+// scheduling builtins exist for the GPU target only, and a kernel template's host-side stub is
+// not emitted when its own body uses them.
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnArgs a) {
+__device__ __forceinline__ void attn_body(const AttnArgs& a) {
   static_assert(D == 64 || D == 128, "head dimension 64 or 128");
   constexpr int KCH = D / 8;                  // 16-byte chunks per key row
   constexpr int KSTEPS = D / 16;              // K16 steps of the score product
   constexpr int DT = D / 32;                  // 32-row tiles of O^T
   constexpr int VROW = kAttnBK + kAttnVPad;   // bf16 per transposed-value row
-  constexpr int KLOADS = kAttnBK * KCH / kAttnThreads;          // 16-byte key loads per thread
+  constexpr int KROWS_DMA = 1024 / (2 * D);   // key rows per 1 KiB DMA instruction
+  constexpr int KDMA = kAttnBK / KROWS_DMA / 4;                 // key DMA instructions per wave
   constexpr int VITEMS = (kAttnBK / 4) * (D / 8);               // (4 keys x 8 dims) value items
-  __shared__ __attribute__((aligned(16))) uint16_t ks[2][kAttnBK * D];
-  __shared__ __attribute__((aligned(16))) uint16_t vt[2][D * VROW];
+  // one __shared__ array per buffer, so the compiler can tell the key DMA into one buffer from
+  // the LDS reads of the other and leaves the DMA in flight across them
+  __shared__ __attribute__((aligned(16))) uint16_t ks0[kAttnBK * D];
+  __shared__ __attribute__((aligned(16))) uint16_t ks1[kAttnBK * D];
+  __shared__ __attribute__((aligned(16))) uint16_t vt0[D * VROW];
+  __shared__ __attribute__((aligned(16))) uint16_t vt1[D * VROW];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31;     // this lane's query within the wave (MFMA column)
   const int hh = lane >> 5;      // MFMA lane half
   const int S = a.S, H = a.H;
   const int nqb = (S + kAttnBQ - 1) / kAttnBQ;
-  const int total = a.B * H * nqb;
-  // XCD-grouped order: each XCD takes a contiguous range (heads of one key/value group), and
-  // inside a head the query blocks with the most keys come first
-  const int item = xcd_tile((int)blockIdx.x, total);
-  const int bh = item / nqb;
-  const int qb = nqb - 1 - (item - bh * nqb);
+  int bh, qb;
+  if (CAUSAL) {
+    // heavy members (query blocks nqb-1 .. nqb-ceil(nqb/2)) of all heads first, then the light
+    // members in the same order: workgroups L and L + (heavy count) are complementary
+    const int hi = (nqb + 1) >> 1;
+    const int lo = nqb >> 1;
+    const int nh = a.B * H * hi;
+    const int L = (int)blockIdx.x;
+    if (L < nh) {
+      bh = L / hi;
+      qb = nqb - 1 - (L - bh * hi);
+    } else {
+      const int J = L - nh;
+      bh = J / lo;
+      qb = J - bh * lo;
+    }
+  } else {
+    const int item = xcd_tile((int)blockIdx.x, a.B * H * nqb);
+    bh = item / nqb;
+    qb = item - bh * nqb;
+  }
   const int b = bh / H;
   const int h = bh - b * H;
   const int g = h / (H / a.Hkv);
@@ -89,39 +112,44 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   // 16-byte chunk swizzle of a key row in LDS: any 16 consecutive keys read at one logical chunk
   // hit 16 distinct bank groups (rows are 256 bytes at D = 128, two rows share 256 bytes at 64)
   auto kswz = [](int key) { return (D == 128) ? (key & 15) : ((key >> 1) & 7); };
-  // global -> registers for one key/value block
-  uint4 kreg[KLOADS];
-  uint4 vreg[4];
-  const bool vitem = tid < VITEMS;
-  const int vkg = tid / (D / 8);               // value item: keys 4vkg..4vkg+3
-  const int vdg = tid - vkg * (D / 8);         //             dims 8vdg..8vdg+7
-  auto load_block = [&](int j0) {
+  // keys: DMA straight into LDS; lane L of a 1 KiB instruction fills physical chunk L % KCH of
+  // key row L / KCH, so it fetches the logical chunk that the swizzle puts there
+  const int dkey = lane / KCH;
+  // per-lane byte offsets within a block (key row krow + dkey of the block; rows at or past S lie
+  // beyond the end of the buffer range and read as zeros, so no per-block test is needed)
+  uint32_t kdma_off[KDMA];
 #pragma unroll
-    for (int i = 0; i < KLOADS; ++i) {
-      const int idx = tid + i * kAttnThreads;
-      const int key = idx / KCH;
-      const int c = idx - key * KCH;
-      const int kp = j0 + key;
-      const uint32_t off = kp < S ? ((uint32_t)kp * (uint32_t)kstride + 8u * c) * 2u : kOOB;
-      kreg[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(kr, off, 0, 0));
-    }
+  for (int i = 0; i < KDMA; ++i) {
+    const int krow = (wave * KDMA + i) * KROWS_DMA;
+    kdma_off[i] = ((uint32_t)(krow + dkey) * (uint32_t)kstride + 8u * (uint32_t)((lane % KCH) ^ kswz(krow + dkey))) * 2u;
+  }
+  const uint32_t kblock_bytes = (uint32_t)kAttnBK * (uint32_t)kstride * 2u;   // one key block
+  auto dma_keys = [&](uint16_t* ks, int jb) {
+    const uint32_t base = (uint32_t)jb * kblock_bytes;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int kp = j0 + 4 * vkg + i;
-      const uint32_t off = (vitem && kp < S) ? ((uint32_t)kp * (uint32_t)kstride + 8u * vdg) * 2u : kOOB;
-      vreg[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(vr, off, 0, 0));
+    for (int i = 0; i < KDMA; ++i) {
+      const int krow = (wave * KDMA + i) * KROWS_DMA;          // first key row of this instruction
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (__attribute__((address_space(3))) void*)(ks + krow * D), 16,
+                                               kdma_off[i] + base, 0, 0, 0);
     }
   };
-  // registers -> LDS buffer `buf`: keys row-major with swizzled 16-byte chunks, values
-  // transposed (row = dimension, 4 consecutive keys per 8-byte write)
-  auto store_block = [&](int buf) {
+  // values: registers, then written transposed (row = dimension, 4 consecutive keys per 8 bytes).
+  // Value item of a thread: keys 4vkg..4vkg+3, dims 8vdg..8vdg+7. In each half-wave the 8-byte
+  // transposed writes of one (dim, key group) slot then cover 4 dim groups x 8 key groups, which
+  // the 68-element row pitch spreads over all 64 LDS banks (dim-group-major lanes conflict 4 ways)
+  uint4 vreg[4];
+  const bool vitem = tid < VITEMS;
+  const int vkg = (tid & 7) + 8 * (tid / (D));  // D / 8 dim groups x 8 key groups per 8 * (D / 8) threads
+  const int vdg = (tid >> 3) & (D / 8 - 1);
+  const uint32_t v_off = ((uint32_t)(4 * vkg) * (uint32_t)kstride + 8u * vdg) * 2u;
+  auto load_values = [&](int jb) {
+    const uint32_t base = (uint32_t)jb * kblock_bytes + v_off;
 #pragma unroll
-    for (int i = 0; i < KLOADS; ++i) {
-      const int idx = tid + i * kAttnThreads;
-      const int key = idx / KCH;
-      const int c = idx - key * KCH;
-      *reinterpret_cast<uint4*>(&ks[buf][key * D + ((c ^ kswz(key)) << 3)]) = kreg[i];
-    }
+    for (int i = 0; i < 4; ++i)
+      vreg[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                              vr, base + (uint32_t)i * (uint32_t)kstride * 2u, 0, 0));
+  };
+  auto store_values = [&](uint16_t* vt) {
     if (vitem) {
       const uint32_t w0[4] = {vreg[0].x, vreg[0].y, vreg[0].z, vreg[0].w};
       const uint32_t w1[4] = {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w};
@@ -135,7 +163,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnArgs a) {
           const uint32_t lo = __builtin_amdgcn_perm(w1[w], w0[w], sel);
           const uint32_t hi = __builtin_amdgcn_perm(w3[w], w2[w], sel);
           const int d = 8 * vdg + 2 * w + e;
-          *reinterpret_cast<uint2*>(&vt[buf][d * VROW + 4 * vkg]) = make_uint2(lo, hi);
+          *reinterpret_cast<uint2*>(&vt[d * VROW + 4 * vkg]) = make_uint2(lo, hi);
         }
       }
     }
@@ -148,86 +176,128 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   f32x16 acc_o[DT];
 #pragma unroll
   for (int i = 0; i < DT; ++i) acc_o[i] = f32x16{};
-  float m_run = -__builtin_inff();
+  float m_run = -__builtin_inff();   // running maximum of the raw scores q.k
   float l_run = 0.0f;
+  const float sl2 = a.sl2;
 
-  load_block(0);
-  store_block(0);
+  dma_keys(ks0, 0);
+  load_values(0);
+  store_values(vt0);
+  wait_vmcnt_lgkm0<0>();
   __syncthreads();
 
-  for (int jb = 0; jb < nkb; ++jb) {
-    const int cur = jb & 1;
-    const int j0 = jb * kAttnBK;
-    if (jb + 1 < nkb) load_block(j0 + kAttnBK);
+  // LDS fragment reads: key rows (A operand of K Q^T) and transposed values (A operand of V^T P^T)
+  auto rd_k = [&](const uint16_t* ksc, int t, int kt) {
+    const int key = kt * 32 + col;
+    const int c = 2 * t + hh;
+    return *reinterpret_cast<const bf16x8*>(&ksc[key * D + ((c ^ kswz(key)) << 3)]);
+  };
+  auto rd_v = [&](const uint16_t* vtc, int u, int dt) {
+    const uint16_t* row = &vtc[(dt * 32 + col) * VROW + 16 * u + 4 * hh];
+    const uint2 lo = *reinterpret_cast<const uint2*>(row);
+    const uint2 hi = *reinterpret_cast<const uint2*>(row + 8);
+    return __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
+  };
 
+  // one key block: math on buffer (ksc, vtc) while the next block's keys stream into (ksn, vtn)
+  auto step = [&](int jb, const uint16_t* ksc, const uint16_t* vtc, uint16_t* ksn, uint16_t* vtn) {
+    const int j0 = jb * kAttnBK;
+    const bool more = jb + 1 < nkb;
+    if (more) {
+      dma_keys(ksn, jb + 1);
+      load_values(jb + 1);
+    }
     if (!CAUSAL || j0 <= wq_last) {
-      // scores S^T[key][query] for the block's 64 keys (two 32-key tiles)
+      // scores S^T[key][query] for the block's 64 keys (two 32-key tiles, interleaved); the key
+      // fragments of step t+2 are read from LDS while the MFMAs of step t run
       f32x16 sc[2] = {f32x16{}, f32x16{}};
+      bf16x8 kf[3][2];
+      kf[0][0] = rd_k(ksc, 0, 0);
+      kf[0][1] = rd_k(ksc, 0, 1);
+      kf[1][0] = rd_k(ksc, 1, 0);
+      kf[1][1] = rd_k(ksc, 1, 1);
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        const int key = kt * 32 + col;
-#pragma unroll
-        for (int t = 0; t < KSTEPS; ++t) {
-          const int c = 2 * t + hh;
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&ks[cur][key * D + ((c ^ kswz(key)) << 3)]);
-          sc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t], sc[kt], 0, 0, 0);
+      for (int t = 0; t < KSTEPS; ++t) {
+        if (t + 2 < KSTEPS) {
+          kf[(t + 2) % 3][0] = rd_k(ksc, t + 2, 0);
+          kf[(t + 2) % 3][1] = rd_k(ksc, t + 2, 1);
         }
+        sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[t % 3][0], qf[t], sc[0], 0, 0, 0);
+        sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[t % 3][1], qf[t], sc[1], 0, 0, 0);
+        if (t + 2 < KSTEPS) QG_SG(kSchedDSRead, 2);
+        QG_SG(kSchedMFMA, 2);
       }
       // key of register r in tile kt: kt*32 + (r/4)*8 + 4hh + r%4
       const bool need_mask = (CAUSAL && j0 + kAttnBK - 1 > q0 + wave * 32) || j0 + kAttnBK > S;
+      if (need_mask) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int kp = j0 + kt * 32 + (r >> 2) * 8 + 4 * hh + (r & 3);
+            if (kp >= S || (CAUSAL && kp > qrow)) sc[kt][r] = -__builtin_inff();
+          }
+      }
       float mloc = -__builtin_inff();
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float x = sc[kt][r] * a.sl2;
-          if (need_mask) {
-            const int kp = j0 + kt * 32 + (r >> 2) * 8 + 4 * hh + (r & 3);
-            if (kp >= S || (CAUSAL && kp > qrow)) x = -__builtin_inff();
-          }
-          sc[kt][r] = x;
-          mloc = fmaxf(mloc, x);
-        }
-      }
+        for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, sc[kt][r]);
       mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
       const float m_new = fmaxf(m_run, mloc);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
+      // p = exp2((s - m) * scale * log2 e), one fused multiply-add per score
+      const float ms = m_new * sl2;
       float lsum = 0.0f;
       uint32_t pf[2][8];   // P^T as packed bf16, per key tile: registers (2i, 2i+1)
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
         for (int r = 0; r < 16; r += 2) {
-          const float p0 = __builtin_amdgcn_exp2f(sc[kt][r] - m_new);
-          const float p1 = __builtin_amdgcn_exp2f(sc[kt][r + 1] - m_new);
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[kt][r], sl2, -ms));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[kt][r + 1], sl2, -ms));
           lsum += p0 + p1;
           pf[kt][r >> 1] = pack_bf16x2(p0, p1);
         }
       }
-      l_run = l_run * alpha + lsum;
+      if (m_new != m_run) {   // rescale the running output only when some row's maximum moved
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * sl2);
+        l_run *= alpha;
 #pragma unroll
-      for (int i = 0; i < DT; ++i) acc_o[i] *= alpha;
+        for (int i = 0; i < DT; ++i) acc_o[i] *= alpha;
+      }
+      m_run = m_new;
+      l_run += lsum;
       // O^T += V^T P^T: K16 step u covers keys 16u..16u+15; lane half hh supplies the keys
-      // 16u + 4hh + {0..3} and 16u + 8 + 4hh + {0..3} (its score registers 8(u%2)..8(u%2)+7)
+      // 16u + 4hh + {0..3} and 16u + 8 + 4hh + {0..3} (its score registers 8(u%2)..8(u%2)+7).
+      // The value fragments of step u+1 are read from LDS while the MFMAs of step u run.
+      bf16x8 vf[2][DT];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) vf[0][dt] = rd_v(vtc, 0, dt);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
+        if (u + 1 < 4) {
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) vf[(u + 1) & 1][dt] = rd_v(vtc, u + 1, dt);
+        }
         const int kt = u >> 1;
         const int r0 = (u & 1) * 4;
         const bf16x8 pb = __builtin_bit_cast(bf16x8, u32x4{pf[kt][r0], pf[kt][r0 + 1], pf[kt][r0 + 2], pf[kt][r0 + 3]});
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const uint16_t* row = &vt[cur][(dt * 32 + col) * VROW + 16 * u + 4 * hh];
-          const uint2 lo = *reinterpret_cast<const uint2*>(row);
-          const uint2 hi = *reinterpret_cast<const uint2*>(row + 8);
-          const bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
-          acc_o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb, acc_o[dt], 0, 0, 0);
-        }
+        for (int dt = 0; dt < DT; ++dt)
+          acc_o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[u & 1][dt], pb, acc_o[dt], 0, 0, 0);
+        if (u + 1 < 4) QG_SG(kSchedDSRead, 2 * DT);
+        QG_SG(kSchedMFMA, DT);
       }
     }
 
-    if (jb + 1 < nkb) store_block(cur ^ 1);
+    if (more) store_values(vtn);
+    wait_vmcnt_lgkm0<0>();   // the key DMA and the value writes are in LDS
     __syncthreads();
+  };
+
+  for (int jb = 0; jb < nkb; jb += 2) {
+    step(jb, ks0, vt0, ks1, vt1);
+    if (jb + 1 < nkb) step(jb + 1, ks1, vt1, ks0, vt0);
   }
 
   // normalise and store: lane (col, hh) holds o[qrow][dt*32 + 8a + 4hh + {0..3}] in acc_o[dt][4a..4a+3]
@@ -245,6 +315,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnArgs a) {
       }
     }
   }
+}
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnArgs a) {
+  attn_body<D, CAUSAL>(a);
 }
 
 }  // namespace qg
