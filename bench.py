@@ -17,7 +17,14 @@ step, with every input resident in HBM. The JSON line also carries the roofline
 of the dominant kernel (per-launch HIP event timing inside the timed region) and
 the CPU oracle's throughput on a bounded sample of the same workload.
 
+Two sections beside the step, not part of ``value``: ``small_m`` (the dense
+projection shapes at M = 1, 4, 16 rows -- decode and speculative verification --
+with weights read from HBM, against the HBM roofline) and ``attention`` (prefill
+flash attention of a 2048-token prompt, 32 query / 4 key-value heads, D=128,
+causal, against the bf16 MFMA peak).
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+       [--small-m-launches L] [--attention-launches L] [--small-m-only] [--attention-only]
 """
 from __future__ import annotations
 
