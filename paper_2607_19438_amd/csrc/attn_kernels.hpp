@@ -9,10 +9,11 @@
 //                  the B columns, held in registers for the whole loop) -- so each lane owns one
 //                  query and 32 of the block's keys, and a row maximum needs one lane exchange;
 //   online softmax on the scores in registers (exp2 with the scale folded into log2 e);
-//   O^T += V^T P^T (the same MFMA: V^T from an LDS copy of the value block transposed at write
-//                  time, P^T straight from the score registers rounded to bf16 -- the score
-//                  layout is the B-operand layout once the MFMA's 16-element K order is chosen
-//                  to match it).
+//   O^T += V^T P^T (the same MFMA: V^T read from the row-major value block with gfx950's
+//                  transposing LDS read, P^T straight from the score registers rounded to bf16
+//                  -- the score layout is the B-operand layout once the MFMA's 16-element K order
+//                  is chosen to match it).
+// Keys and values both go from HBM to LDS by DMA, with no register staging.
 // Rows are normalised by the running sum at the end and stored as bf16. Causal blocks above the
 // diagonal are skipped; blocks on it are masked key by key.
 #pragma once
@@ -24,7 +25,6 @@ namespace qg {
 constexpr int kAttnThreads = 256;   // four waves
 constexpr int kAttnBQ = 128;        // query rows per workgroup
 constexpr int kAttnBK = 64;         // keys per block
-constexpr int kAttnVPad = 4;        // bf16 padding of a transposed-value LDS row (bank spread)
 
 struct AttnArgs {
   const uint16_t* q;   // bf16 [B][S][H][D]
@@ -47,16 +47,14 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   constexpr int KCH = D / 8;                  // 16-byte chunks per key row
   constexpr int KSTEPS = D / 16;              // K16 steps of the score product
   constexpr int DT = D / 32;                  // 32-row tiles of O^T
-  constexpr int VROW = kAttnBK + kAttnVPad;   // bf16 per transposed-value row
   constexpr int KROWS_DMA = 1024 / (2 * D);   // key rows per 1 KiB DMA instruction
   constexpr int KDMA = kAttnBK / KROWS_DMA / 4;                 // key DMA instructions per wave
-  constexpr int VITEMS = (kAttnBK / 4) * (D / 8);               // (4 keys x 8 dims) value items
   // one __shared__ array per buffer, so the compiler can tell the key DMA into one buffer from
   // the LDS reads of the other and leaves the DMA in flight across them
   __shared__ __attribute__((aligned(16))) uint16_t ks0[kAttnBK * D];
   __shared__ __attribute__((aligned(16))) uint16_t ks1[kAttnBK * D];
-  __shared__ __attribute__((aligned(16))) uint16_t vt0[D * VROW];
-  __shared__ __attribute__((aligned(16))) uint16_t vt1[D * VROW];
+  __shared__ __attribute__((aligned(16))) uint16_t vt0[kAttnBK * D];
+  __shared__ __attribute__((aligned(16))) uint16_t vt1[kAttnBK * D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -133,39 +131,24 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
                                                kdma_off[i] + base, 0, 0, 0);
     }
   };
-  // values: registers, then written transposed (row = dimension, 4 consecutive keys per 8 bytes).
-  // Value item of a thread: keys 4vkg..4vkg+3, dims 8vdg..8vdg+7. In each half-wave the 8-byte
-  // transposed writes of one (dim, key group) slot then cover 4 dim groups x 8 key groups, which
-  // the 68-element row pitch spreads over all 64 LDS banks (dim-group-major lanes conflict 4 ways)
-  uint4 vreg[4];
-  const bool vitem = tid < VITEMS;
-  const int vkg = (tid & 7) + 8 * (tid / (D));  // D / 8 dim groups x 8 key groups per 8 * (D / 8) threads
-  const int vdg = (tid >> 3) & (D / 8 - 1);
-  const uint32_t v_off = ((uint32_t)(4 * vkg) * (uint32_t)kstride + 8u * vdg) * 2u;
-  auto load_values = [&](int jb) {
-    const uint32_t base = (uint32_t)jb * kblock_bytes + v_off;
+  // values: DMA straight into LDS too, row-major (key rows), 16-byte chunks XOR-swizzled by
+  // vswz(key); the output product reads them with the transposing LDS read, which hands each
+  // lane 4 keys of one dimension. The swizzle puts the 4 consecutive keys x 64 bytes that the
+  // 32 lanes of one half-wave read on 256 distinct bytes of the bank space.
+  auto vswz = [](int key) { return (D == 128) ? 4 * (key & 3) : 4 * ((key >> 1) & 1); };
+  uint32_t vdma_off[KDMA];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      vreg[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                                              vr, base + (uint32_t)i * (uint32_t)kstride * 2u, 0, 0));
-  };
-  auto store_values = [&](uint16_t* vt) {
-    if (vitem) {
-      const uint32_t w0[4] = {vreg[0].x, vreg[0].y, vreg[0].z, vreg[0].w};
-      const uint32_t w1[4] = {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w};
-      const uint32_t w2[4] = {vreg[2].x, vreg[2].y, vreg[2].z, vreg[2].w};
-      const uint32_t w3[4] = {vreg[3].x, vreg[3].y, vreg[3].z, vreg[3].w};
+  for (int i = 0; i < KDMA; ++i) {
+    const int krow = (wave * KDMA + i) * KROWS_DMA;
+    vdma_off[i] = ((uint32_t)(krow + dkey) * (uint32_t)kstride + 8u * (uint32_t)((lane % KCH) ^ vswz(krow + dkey))) * 2u;
+  }
+  auto dma_values = [&](uint16_t* vs, int jb) {
+    const uint32_t base = (uint32_t)jb * kblock_bytes;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const uint32_t sel = e ? 0x07060302u : 0x05040100u;   // high or low halves of two dwords
-          const uint32_t lo = __builtin_amdgcn_perm(w1[w], w0[w], sel);
-          const uint32_t hi = __builtin_amdgcn_perm(w3[w], w2[w], sel);
-          const int d = 8 * vdg + 2 * w + e;
-          *reinterpret_cast<uint2*>(&vt[d * VROW + 4 * vkg]) = make_uint2(lo, hi);
-        }
-      }
+    for (int i = 0; i < KDMA; ++i) {
+      const int krow = (wave * KDMA + i) * KROWS_DMA;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (__attribute__((address_space(3))) void*)(vs + krow * D), 16,
+                                               vdma_off[i] + base, 0, 0, 0);
     }
   };
 
@@ -181,8 +164,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   const float sl2 = a.sl2;
 
   dma_keys(ks0, 0);
-  load_values(0);
-  store_values(vt0);
+  dma_values(vt0, 0);
   wait_vmcnt_lgkm0<0>();
   __syncthreads();
 
@@ -192,11 +174,28 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
     const int c = 2 * t + hh;
     return *reinterpret_cast<const bf16x8*>(&ksc[key * D + ((c ^ kswz(key)) << 3)]);
   };
+  // V^T fragment of MFMA step u, tile dt: lane (d = col, hh) needs the keys 16u + 4hh + {0..3}
+  // and 16u + 8 + 4hh + {0..3} of dimension 32dt + col. In a transposing read each 16-lane group
+  // returns, to lane i, element i % 4 of the 8-byte pieces that lanes 4r + i/4 (r = 0..3) point
+  // at; so lane s of the group points at key (run start + s/4), dimensions 4(s%4)..+3 of the
+  // group's 16, and lane i gets the run's 4 keys of dimension (group's first) + i.
+  const int trk = (lane & 15) >> 2;                   // key within the run of 4
+  const int trd = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);   // first of the 4 dims this lane points at
   auto rd_v = [&](const uint16_t* vtc, int u, int dt) {
-    const uint16_t* row = &vtc[(dt * 32 + col) * VROW + 16 * u + 4 * hh];
-    const uint2 lo = *reinterpret_cast<const uint2*>(row);
-    const uint2 hi = *reinterpret_cast<const uint2*>(row + 8);
-    return __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
+    uint32_t w[4];
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int key = 16 * u + 8 * half + 4 * hh + trk;
+      const int dim = 32 * dt + trd;
+      const int e = key * D + (((dim >> 3) ^ vswz(key)) << 3) + (dim & 7);
+      typedef short v4i16 __attribute__((ext_vector_type(4)));
+      const v4i16 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) v4i16*)(const_cast<uint16_t*>(vtc) + e));
+      const uint2 rr = __builtin_bit_cast(uint2, r);
+      w[2 * half] = rr.x;
+      w[2 * half + 1] = rr.y;
+    }
+    return __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
   };
 
   // one key block: math on buffer (ksc, vtc) while the next block's keys stream into (ksn, vtn)
@@ -205,7 +204,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
     const bool more = jb + 1 < nkb;
     if (more) {
       dma_keys(ksn, jb + 1);
-      load_values(jb + 1);
+      dma_values(vtn, jb + 1);
     }
     if (!CAUSAL || j0 <= wq_last) {
       // scores S^T[key][query] for the block's 64 keys (two 32-key tiles, interleaved); the key
@@ -290,8 +289,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
       }
     }
 
-    if (more) store_values(vtn);
-    wait_vmcnt_lgkm0<0>();   // the key DMA and the value writes are in LDS
+    wait_vmcnt_lgkm0<0>();   // the key and value DMA of the next block are in LDS
     __syncthreads();
   };
 
