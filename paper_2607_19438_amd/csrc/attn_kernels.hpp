@@ -41,6 +41,14 @@ struct AttnArgs {
 // The kernel body lives in a device function (the kernel below only forwards to it): its
 // scheduling builtins exist for the GPU target only, and a kernel template's host-side stub is
 // not emitted when its own body uses them.
+// The value of lane l ^ 32 (the other MFMA lane half of the same query), with one VALU lane swap.
+__device__ __forceinline__ float other_half(float x) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);   // {x[l % 32], x[32 + l % 32]}
+  const int lane = (int)(threadIdx.x & 63);
+  return __builtin_bit_cast(float, (unsigned)(lane < 32 ? r[1] : r[0]));
+}
+
 template <int D, bool CAUSAL>
 __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   static_assert(D == 64 || D == 128, "head dimension 64 or 128");
@@ -242,14 +250,24 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, sc[kt][r]);
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+      mloc = fmaxf(mloc, other_half(mloc));
       const float m_new = fmaxf(m_run, mloc);
-      // p = exp2((s - m) * scale * log2 e), one fused multiply-add per score
+      // rescale the running output only when some row's maximum moved (before any of this
+      // block's output-product MFMAs)
+      if (m_new != m_run) {
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * sl2);
+        l_run *= alpha;
+#pragma unroll
+        for (int i = 0; i < DT; ++i) acc_o[i] *= alpha;
+      }
+      m_run = m_new;
+      // p = exp2((s - m) * scale * log2 e), one fused multiply-add per score; P^T as packed bf16,
+      // per key tile: registers (2i, 2i+1). Tile 1's exponentials are written between the
+      // output-product MFMAs of tile 0 so the two overlap.
       const float ms = m_new * sl2;
       float lsum = 0.0f;
-      uint32_t pf[2][8];   // P^T as packed bf16, per key tile: registers (2i, 2i+1)
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
+      uint32_t pf[2][8];
+      auto exp_tile = [&](int kt) {
 #pragma unroll
         for (int r = 0; r < 16; r += 2) {
           const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[kt][r], sl2, -ms));
@@ -257,15 +275,8 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
           lsum += p0 + p1;
           pf[kt][r >> 1] = pack_bf16x2(p0, p1);
         }
-      }
-      if (m_new != m_run) {   // rescale the running output only when some row's maximum moved
-        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * sl2);
-        l_run *= alpha;
-#pragma unroll
-        for (int i = 0; i < DT; ++i) acc_o[i] *= alpha;
-      }
-      m_run = m_new;
-      l_run += lsum;
+      };
+      exp_tile(0);
       // O^T += V^T P^T: K16 step u covers keys 16u..16u+15; lane half hh supplies the keys
       // 16u + 4hh + {0..3} and 16u + 8 + 4hh + {0..3} (its score registers 8(u%2)..8(u%2)+7).
       // The value fragments of step u+1 are read from LDS while the MFMAs of step u run.
@@ -284,9 +295,9 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
           acc_o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[u & 1][dt], pb, acc_o[dt], 0, 0, 0);
-        if (u + 1 < 4) QG_SG(kSchedDSRead, 2 * DT);
-        QG_SG(kSchedMFMA, DT);
+        if (u == 0) exp_tile(1);
       }
+      l_run += lsum;
     }
 
     wait_vmcnt_lgkm0<0>();   // the key and value DMA of the next block are in LDS
@@ -299,7 +310,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   }
 
   // normalise and store: lane (col, hh) holds o[qrow][dt*32 + 8a + 4hh + {0..3}] in acc_o[dt][4a..4a+3]
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = l_run + other_half(l_run);
   const float inv = 1.0f / l_tot;
   if (qrow < S) {
     uint16_t* orow = a.o + ((size_t)b * S + qrow) * qstride + (size_t)h * D;
