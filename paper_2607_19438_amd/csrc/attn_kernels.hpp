@@ -116,8 +116,10 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   }
 
   // 16-byte chunk swizzle of a key row in LDS: any 16 consecutive keys read at one logical chunk
-  // hit 16 distinct bank groups (rows are 256 bytes at D = 128, two rows share 256 bytes at 64)
-  auto kswz = [](int key) { return (D == 128) ? (key & 15) : ((key >> 1) & 7); };
+  // hit 16 distinct bank groups, and any 8 hit 8 distinct 16-byte groups of a 128-byte bank
+  // window (rows are 256 bytes at D = 128; at D = 64 the rows are 128 bytes, the layout of the
+  // GEMM tiles, and take their row swizzle)
+  auto kswz = [](int key) { return (D == 128) ? (key & 15) : row_swizzle(key); };
   // keys: DMA straight into LDS; lane L of a 1 KiB instruction fills physical chunk L % KCH of
   // key row L / KCH, so it fetches the logical chunk that the swizzle puts there
   const int dkey = lane / KCH;
@@ -223,6 +225,9 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
       kf[0][1] = rd_k(ksc, 0, 1);
       kf[1][0] = rd_k(ksc, 1, 0);
       kf[1][1] = rd_k(ksc, 1, 1);
+      // raised wave priority while a wave issues its MFMAs: the SIMD's other wave fills the
+      // issue slots between them with its softmax VALU work
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int t = 0; t < KSTEPS; ++t) {
         if (t + 2 < KSTEPS) {
@@ -234,6 +239,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
         if (t + 2 < KSTEPS) QG_SG(kSchedDSRead, 2);
         QG_SG(kSchedMFMA, 2);
       }
+      __builtin_amdgcn_s_setprio(0);
       // key of register r in tile kt: kt*32 + (r/4)*8 + 4hh + r%4
       const bool need_mask = (CAUSAL && j0 + kAttnBK - 1 > q0 + wave * 32) || j0 + kAttnBK > S;
       if (need_mask) {
@@ -252,19 +258,23 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
         for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, sc[kt][r]);
       mloc = fmaxf(mloc, other_half(mloc));
       const float m_new = fmaxf(m_run, mloc);
-      // rescale the running output only when some row's maximum moved (before any of this
-      // block's output-product MFMAs)
-      if (m_new != m_run) {
+      // The reference maximum m_run moves (and the running output and sum are rescaled, before
+      // any of this block's output-product MFMAs) only when the block's maximum exceeds it by
+      // more than 8 in exp2 units. Softmax does not depend on the reference as long as the
+      // weights and their sum use the same one, and the threshold keeps every weight <= 2^8,
+      // far inside fp32 and bf16 range; most blocks skip the rescale. (The first block always
+      // moves it from -inf, with alpha = 0 on the empty sum.)
+      if ((m_new - m_run) * sl2 > 8.0f) {
         const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * sl2);
         l_run *= alpha;
 #pragma unroll
         for (int i = 0; i < DT; ++i) acc_o[i] *= alpha;
+        m_run = m_new;
       }
-      m_run = m_new;
       // p = exp2((s - m) * scale * log2 e), one fused multiply-add per score; P^T as packed bf16,
       // per key tile: registers (2i, 2i+1). Tile 1's exponentials are written between the
       // output-product MFMAs of tile 0 so the two overlap.
-      const float ms = m_new * sl2;
+      const float ms = m_run * sl2;
       float lsum = 0.0f;
       uint32_t pf[2][8];
       auto exp_tile = [&](int kt) {
@@ -283,6 +293,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
       bf16x8 vf[2][DT];
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) vf[0][dt] = rd_v(vtc, 0, dt);
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         if (u + 1 < 4) {
@@ -297,6 +308,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
           acc_o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[u & 1][dt], pb, acc_o[dt], 0, 0, 0);
         if (u == 0) exp_tile(1);
       }
+      __builtin_amdgcn_s_setprio(0);
       l_run += lsum;
     }
 

@@ -43,13 +43,22 @@ __device__ __forceinline__ float fp16_to_f32(uint16_t h) {
   return (float)__builtin_bit_cast(_Float16, h);
 }
 
+// Row swizzle of the 16-byte chunks of a [rows][64] bf16 LDS tile: logical chunk c of row r
+// sits at slot c ^ row_swizzle(r). The map is linear over GF(2) in the low four row bits (bits
+// 0..3 map to 1, 3, 5, 1; table below, one nibble per r mod 16). It keeps every access of the
+// tile kernel free of bank conflicts whether a 16-byte LDS access phase serves 16 lanes over 64
+// four-byte banks or 8 lanes over 32 banks:
+//   fragment reads: 32 consecutive rows at one logical chunk (per lane half);
+//   Q4 dequant writes: lane t writes row t / 2, chunk 4 (t % 2) + u;
+//   Q8 dequant writes: lane t writes row t / 4, chunk 2 (t % 4) + u.
+// (A swizzle by the row pair, (r >> 1) & 7, is conflict-free only in the first model; the
+// hardware counters show the second.)
+constexpr unsigned long long kRowSwizzleTable = 0x6754320176452310ull;
+__host__ __device__ constexpr int row_swizzle(int r) { return (int)((kRowSwizzleTable >> (4 * (r & 15))) & 7); }
+
 // Byte offset of 16-byte chunk `c` (0..7) of row `r` in a [rows][64] bf16 LDS tile.
-// LDS has 64 four-byte banks (256 bytes), i.e. two 128-byte tile rows. Chunks are
-// XOR-swizzled by the row pair (r >> 1), so any 16 consecutive rows read at the
-// same logical chunk land on 16 distinct 16-byte bank groups (the 16 lanes that
-// one ds_read_b128 phase serves), and 4 rows x 4 even (or odd) chunks do too.
 __device__ __forceinline__ int lds_chunk(int r, int c) {
-  return r * kRowBytes + ((c ^ ((r >> 1) & 7)) << 4);
+  return r * kRowBytes + ((c ^ row_swizzle(r)) << 4);
 }
 
 // 16 int8 weights (one 16-byte load) -> 16 bf16 = w * s, as 8 packed dwords.
@@ -127,6 +136,10 @@ __device__ __forceinline__ void wait_vmcnt_lgkm0() {
 
 // s_waitcnt lgkmcnt(0) only (vector memory loads stay in flight)
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
+
+#ifndef QG_XPREFETCH
+#define QG_XPREFETCH 1
+#endif
 
 #ifndef QG_PINGPONG
 #define QG_PINGPONG 1
@@ -298,7 +311,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
 #pragma unroll
   for (int j = 0; j < XL; ++j) {
     const int r = (xw * XL + j) * 8 + (lane >> 3);
-    dma_c[j] = (lane & 7) ^ ((r >> 1) & 7);     // the chunk that lds_chunk(r, .) places at slot lane & 7
+    dma_c[j] = (lane & 7) ^ row_swizzle(r);     // the chunk that lds_chunk(r, .) places at slot lane & 7
   }
   if constexpr (MOE) {
     xr = make_rsrc(a.x, (uint32_t)a.T * (uint32_t)K * 2u);
@@ -371,6 +384,27 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     }
   };
 
+  // L2 prefetch of the gathered activation rows two steps ahead (MoE ping-pong DMA waves): DMA wave xw touches the
+  // 128-byte row segment of tile rows xw * BM / 4 + lane with one 4-byte LDS-DMA load into a dummy
+  // LDS area (never read), so that the segment is in L2 by the time the real DMA of that step is
+  // issued, one step later. A load into a register would do the same, but the compiler would wait
+  // for it as soon as the register is reused.
+  constexpr bool XPF = PP && MOE && QG_XPREFETCH;   // dense rows are contiguous: no gain measured there
+  uint32_t pfoff = kOOB;
+  if constexpr (XPF) {
+    constexpr int kRowsPerWave = BM / 4;
+    const int r = xw * kRowsPerWave + lane;
+    if (lane < kRowsPerWave && r < rows_valid) {
+      const int src = MOE ? s_xrow[r] : r;
+      if (src >= 0) pfoff = (uint32_t)src * (uint32_t)K * 2u;
+    }
+  }
+  auto prefetch_x = [&](int kt_local) {
+    const uint32_t off = (pfoff == kOOB || kt_local >= nk) ? kOOB : pfoff + (uint32_t)(ks0 + kt_local) * (uint32_t)kRowBytes;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)st.x[2], 4, off, 0, 0, 0);
+  };
+  constexpr int kPF = XPF ? 1 : 0;   // prefetch loads per DMA-wave step
+
   // weight register sets: the loads of step k are issued kWD steps ahead, into set k % kWD
   uint4 wv[kWD][WC];
   uint32_t sv[kWD][WC];
@@ -425,13 +459,13 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   const int lr = lane & 31;
   const int lh = lane >> 5;
   // per-lane LDS byte offsets of the A / B fragments of sub-step 0 (chunk lh); chunk 2 kk + lh
-  // of row r sits at r * 128 + (((2 kk + lh) ^ ((r >> 1) & 7)) << 4)
+  // of row r sits at r * 128 + (((2 kk + lh) ^ row_swizzle(r)) << 4)
   int aoff[KT::kTM], boff[KT::kTN];
 #pragma unroll
   for (int i = 0; i < KT::kTM; ++i) aoff[i] = ((i * WM + wm) * 32 + lr) * kRowBytes;
 #pragma unroll
   for (int j = 0; j < KT::kTN; ++j) boff[j] = (wn * KT::kWTN + j * 32 + lr) * kRowBytes;
-  const int rsw = ((lr >> 1) & 7);   // (r >> 1) & 7 is the same for every fragment row: bases are multiples of 32
+  const int rsw = row_swizzle(lr);   // the same for every fragment row: bases are multiples of 32 (16 would do)
 
   // Fragment registers: sub-step kk uses set kk & 1. The last sub-step's MFMAs run after
   // the barrier that closes the K step, overlapping the next step's first LDS reads.
@@ -646,6 +680,10 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       __builtin_amdgcn_sched_barrier(0);                   // the wait below counts the loads after the DMA
       issue_w(kt + kWD, wv[wset_issue], sv[wset_issue], CD);
       __builtin_amdgcn_sched_barrier(0);
+      if constexpr (XPF) {
+        prefetch_x(kt + 2);
+        __builtin_amdgcn_sched_barrier(0);
+      }
 #pragma unroll
       for (int u = 0; u < CD * kUnitsPerChunk; ++u)
         dequant_unit(kt + 1, u, wv[wset_next], sv[wset_next], ws_cur ^ 1);
@@ -654,8 +692,8 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       mfma_phase(xs_cur, ws_cur, true);
       // this wave's activation DMA of step kt+1: the only vector-memory loads issued after it are
       // its weight loads of step kt+kWD, counted only when live (loads of steps past the last one
-      // may be deleted, and an undercount only makes the wait stricter)
-      if (kt + kWD <= nk) wait_vmcnt_lgkm0<2 * CD>(); else wait_vmcnt_lgkm0<0>();
+      // may be deleted, and an undercount only makes the wait stricter), and its prefetch load
+      if (kt + kWD <= nk) wait_vmcnt_lgkm0<2 * CD + kPF>(); else wait_vmcnt_lgkm0<0>();
       __builtin_amdgcn_s_barrier();
     };
     int kt = 0;
@@ -839,7 +877,7 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
   using KT = TileKernel<FMT, BM, BN, WM, WN, false, XS>;
   __shared__ __attribute__((aligned(1024))) char lx0[KT::kXTileBytes];
   __shared__ __attribute__((aligned(1024))) char lx1[KT::kXTileBytes];
-  __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 16];
+  __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 256];
   __shared__ __attribute__((aligned(1024))) char lw0[KT::kWTileBytes];
   __shared__ __attribute__((aligned(1024))) char lw1[KT::kWTileBytes];
   const LdsStages lds{{lx0, lx1, XS == 3 ? lx2 : nullptr}, {lw0, lw1}};
@@ -872,7 +910,7 @@ __global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtr
   static_assert(KT::kThreads >= kMaxExpertsPerLaunch, "the tile prefix needs one lane per expert");
   __shared__ __attribute__((aligned(1024))) char lx0[KT::kXTileBytes];
   __shared__ __attribute__((aligned(1024))) char lx1[KT::kXTileBytes];
-  __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 16];
+  __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 256];
   __shared__ __attribute__((aligned(1024))) char lw0[KT::kWTileBytes];
   __shared__ __attribute__((aligned(1024))) char lw1[KT::kWTileBytes];
   const LdsStages lds{{lx0, lx1, XS == 3 ? lx2 : nullptr}, {lw0, lw1}};
