@@ -17,14 +17,16 @@ step, with every input resident in HBM. The JSON line also carries the roofline
 of the dominant kernel (per-launch HIP event timing inside the timed region) and
 the CPU oracle's throughput on a bounded sample of the same workload.
 
-Two sections beside the step, not part of ``value``: ``small_m`` (the dense
+Three sections beside the step, not part of ``value``: ``small_m`` (the dense
 projection shapes at M = 1, 4, 16 rows -- decode and speculative verification --
-with weights read from HBM, against the HBM roofline) and ``attention`` (prefill
-flash attention of a 2048-token prompt, 32 query / 4 key-value heads, D=128,
-causal, against the bf16 MFMA peak).
+with weights read from HBM, against the HBM roofline), ``moe_t128`` (the skewed MoE
+FFN at a 128-token prompt, the HBM-bound tail of the MoE path, weights read from HBM,
+against the HBM roofline) and ``attention`` (prefill flash attention of a 2048-token
+prompt, 32 query / 4 key-value heads, D=128, causal, against the bf16 MFMA peak).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-       [--small-m-launches L] [--attention-launches L] [--small-m-only] [--attention-only]
+       [--small-m-launches L] [--attention-launches L] [--moe-t128-launches L]
+       [--small-m-only] [--attention-only] [--moe-t128-only]
 """
 from __future__ import annotations
 
@@ -60,6 +62,9 @@ def parse():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (for scaling HBM byte counters) and exit")
     ap.add_argument("--only", default="", help="comma list of parts to run: dense_gate_up,dense_down,moe_t2048,moe_t8192")
+    ap.add_argument("--moe-t128-launches", type=int, default=50,
+                    help="launches per projection of the T=128 MoE section (0: skip it)")
+    ap.add_argument("--moe-t128-only", action="store_true", help="run only the T=128 MoE section and print its JSON")
     ap.add_argument("--small-m-launches", type=int, default=200,
                     help="launches per small-M (decode / verification) case; 0 skips that section")
     ap.add_argument("--attention-launches", type=int, default=50,
@@ -245,6 +250,79 @@ def small_m_section(torch, q, synth, launches):
             "cases": rows}
 
 
+# The skewed MoE FFN of the T=8192 workload at a 128-token prompt: 1024 token slots over the
+# active experts only, so every projection reads each active expert's packed weights about once
+# for a few rows -- the HBM-bound tail of the MoE path. Reported beside the step, not part of
+# `value`, against the HBM roofline.
+MOE_T128_COPIES = 4        # expert weight sets cycled: 4 x ~135 MB of active experts > the 256 MiB last-level cache
+
+
+def moe_t128_section(torch, q, synth, launches):
+    """Per-launch time of the T=128 skewed MoE projections, weights read from HBM (sets rotated)."""
+    dev = torch.device("cuda:0")
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    (case,) = synth.config(4, T_override=128)
+    r = case.routing
+    A = case.T * case.topk
+    counts = np.diff(r.expert_offsets)
+    active = int((counts > 0).sum())
+    x = torch.from_numpy(np.ascontiguousarray(case.x).view(np.int16)).view(torch.bfloat16).to(dev)
+    idx = torch.from_numpy(r.token_expert_idx).to(dev)
+    off = torch.from_numpy(r.expert_offsets).to(dev)
+    rw = torch.from_numpy(r.route_w).to(dev)
+    wgu = torch.from_numpy(np.stack([w.wq for w in case.w_gate_up])).to(dev)
+    sgu = torch.from_numpy(np.stack([w.scales for w in case.w_gate_up])).to(dev)
+    wd = torch.from_numpy(np.stack([w.wq for w in case.w_down])).to(dev)
+    sd = torch.from_numpy(np.stack([w.scales for w in case.w_down])).to(dev)
+    sets = [(q.ExpertTable(wgu.clone(), sgu.clone(), case.fmt), q.ExpertTable(wd.clone(), sd.clone(), case.fmt))
+            for _ in range(MOE_T128_COPIES)]
+    perm = q.moe_bucket(idx, off)
+    h = torch.empty((A, case.inter), dtype=torch.bfloat16, device=dev)
+    y2 = torch.empty((A, case.hidden), dtype=torch.float32, device=dev)
+    out = torch.empty((case.T, case.hidden), dtype=torch.float32, device=dev)
+    gate_up = lambda i: q.moe_gate_up_swiglu(x, perm, off, sets[i % MOE_T128_COPIES][0], None, case.topk, case.fmt,
+                                             out=h)
+    down = lambda i: q.moe_grouped(h, perm, off, sets[i % MOE_T128_COPIES][1], None, 1, case.fmt, out=y2)
+
+    def ffn(i):
+        q.moe_bucket(idx, off, out=perm)
+        gate_up(i)
+        down(i)
+        q.moe_combine(y2, rw, case.topk, out=out)
+
+    def per_launch(fn):
+        for i in range(2 * MOE_T128_COPIES):
+            fn(i)
+        torch.cuda.synchronize()
+        first, last = ev(), ev()
+        first.record()
+        for i in range(launches):
+            fn(i)
+        last.record()
+        torch.cuda.synchronize()
+        return first.elapsed_time(last) / launches * 1e3
+
+    us_gu, us_dn, us_ffn = per_launch(gate_up), per_launch(down), per_launch(ffn)
+    packed = lambda n, k: n * k // 2 + n * (k // 32) * 2       # Q4 bytes + fp16 scales of one expert
+    b_gu = active * packed(2 * case.inter, case.hidden) + 2 * case.T * case.hidden + 2 * A * case.inter
+    b_dn = active * packed(case.hidden, case.inter) + 2 * A * case.inter + 4 * A * case.hidden
+    rows = []
+    for name, us, nbytes, flops in (("gate_up+SiLU", us_gu, b_gu, case.flops_gate_up),
+                                    ("down", us_dn, b_dn, case.flops_down)):
+        rows.append({"projection": name, "us_per_launch": us, "bytes_per_launch": nbytes,
+                     "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_hbm": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+                     "TFLOP/s": flops / (us * 1e-6) / 1e12})
+        log(f"MoE T=128 {name}: {us:.1f} us/launch, {rows[-1]['GB/s']:.0f} GB/s")
+    log(f"MoE T=128 FFN (bucketing, both projections, combine): {us_ffn:.1f} us")
+    del sets
+    torch.cuda.empty_cache()
+    return {"workload": "MoE Q4 FFN T=128 E=128 top8 Zipf-skewed (hidden 2048, expert inter 768)",
+            "active_experts": active, "rows_per_active_expert": [int(counts[counts > 0].min()),
+                                                                 int(counts[counts > 0].max())],
+            "bound": "hbm", "peak": PEAK_HBM_GBS, "unit": "GB/s", "weight_sets_rotated": MOE_T128_COPIES,
+            "projections": rows, "ffn_us_per_launch": us_ffn, "launches": launches}
+
+
 def attention_section(torch, q, synth, launches):
     """Prefill attention of the MoE model family's layer (S=2048, 32/4 heads, D=128, causal)."""
     dev = torch.device("cuda:0")
@@ -360,6 +438,9 @@ def main():
     if args.small_m_only:
         print(json.dumps({"small_m": small_m_section(torch, q, synth, args.small_m_launches)}), flush=True)
         return 0
+    if args.moe_t128_only:
+        print(json.dumps({"moe_t128": moe_t128_section(torch, q, synth, args.moe_t128_launches)}), flush=True)
+        return 0
     log("generating inputs")
     t0 = time.perf_counter()
     parts = build_parts(torch, q, synth, args.only, fused=not args.unfused)
@@ -418,6 +499,11 @@ def main():
         log("small-M (decode / verification) cases")
         small = small_m_section(torch, q, synth, args.small_m_launches)
 
+    t128 = None
+    if args.moe_t128_launches > 0 and not args.only:
+        log("MoE FFN at T=128 (HBM-bound tail)")
+        t128 = moe_t128_section(torch, q, synth, args.moe_t128_launches)
+
     attn = None
     if args.attention_launches > 0 and not args.only:
         log("prefill attention")
@@ -442,6 +528,7 @@ def main():
         "breakdown": breakdown,
         "small_m": small,
         "attention": attn,
+        "moe_t128": t128,
     }
     print(json.dumps(line), flush=True)
     return 0
