@@ -183,11 +183,14 @@ class EventTimer:
 
         return _Ctx()
 
-    def summary(self):
+    def times(self):
         out = {}
         for name, s, e in self.pending:
             out.setdefault(name, []).append(s.elapsed_time(e))
-        return {k: float(np.mean(v)) for k, v in out.items()}
+        return out
+
+    def summary(self):
+        return {k: float(np.mean(v)) for k, v in self.times().items()}
 
 
 # Small-M (decode / speculative verification) cases: the prefill projection shapes at M <= 16
@@ -480,12 +483,15 @@ def main():
             run_part(q, p, timer)
     torch.cuda.synchronize()
     wall_ev = time.perf_counter() - t1
-    per = timer.summary()
+    per_all = timer.times()
+    per = {k: float(np.mean(v)) for k, v in per_all.items()}
     flops_of = {}
     for p in parts:
         for k, f in p.gemm_flops.items():
             flops_of[f"{p.name}:{k}"] = f
-    breakdown = {k: {"ms": per[k], "tflops": flops_of[k] / (per[k] * 1e-3) / 1e12,
+    breakdown = {k: {"ms": per[k], "median_ms": float(np.median(per_all[k])),
+                     "p90_ms": float(np.percentile(per_all[k], 90)),
+                     "tflops": flops_of[k] / (per[k] * 1e-3) / 1e12,
                      "frac_mfma": flops_of[k] / (per[k] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS} for k in per}
     dom = max(per, key=lambda k: per[k])
     achieved = flops_of[dom] / (per[dom] * 1e-3) / 1e12
