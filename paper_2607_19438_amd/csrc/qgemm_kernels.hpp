@@ -145,6 +145,12 @@ __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (
 #define QG_PINGPONG 1
 #endif
 
+// Groups the ping-pong DMA-role step splits its activation DMA into, each followed by a share of
+// its dequantisation (0: all loads first, then all dequantisation)
+#ifndef QG_VMEM_SPLIT
+#define QG_VMEM_SPLIT 2
+#endif
+
 // ---------------------------------------------------------------------------
 // tile kernel
 // ---------------------------------------------------------------------------
@@ -218,7 +224,7 @@ typedef __attribute__((address_space(3))) char lds_char;
 // the compiler can tell they do not alias and keeps the DMA in flight across them instead of
 // draining it (vmcnt) before every LDS access.
 struct LdsStages {
-  char* x[3];
+  char* x[3];   // activation stages; x[2] is null with two stages (see the activation prefetch)
   char* w[2];
 };
 
@@ -275,6 +281,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   // with its partner's memory and VALU work in the other issue slots, instead of both waves
   // arriving at one barrier at different times.
   constexpr bool PP = QG_PINGPONG && WM == 2 && WN == 4 && XS == 2;
+  constexpr int kVmemSplit = QG_VMEM_SPLIT;
   constexpr int XL = PP ? 2 * KT::kXLoads : KT::kXLoads;        // DMA loads per DMA-role wave
   // Weight chunks per thread: without ping-pong every thread takes kWChunks. With it the wm = 0
   // waves take CQ chunks (dequantised after their MFMA phase) and the wm = 1 waves CD chunks
@@ -367,12 +374,13 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   // Loads of steps past this tile's last one (kt_local >= nk) are issued with out-of-range
   // offsets: the buffer range check answers them with zeros, no memory is read, and the K loop
   // stays free of branches around its loads.
-  auto issue_x = [&](int kt_local, int stage) {
+  auto issue_x = [&](int kt_local, int stage, int j0 = 0, int j1 = 1 << 30) {
     const int kt = ks0 + kt_local;
     const uint32_t kbyte = (uint32_t)kt * (uint32_t)kRowBytes;
     const bool tail = (kt + 1) * kBK > K || kt_local >= nk;
 #pragma unroll
     for (int j = 0; j < XL; ++j) {
+      if (j < j0 || j >= j1) continue;
       // an 8-row group wholly past the valid rows is not fetched at all: its LDS rows keep
       // stale data, which only reaches accumulator rows that are never stored. (With three
       // stages the waits count this step's activation loads, so every group is issued.)
@@ -384,11 +392,13 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     }
   };
 
-  // L2 prefetch of the gathered activation rows two steps ahead (MoE ping-pong DMA waves): DMA wave xw touches the
-  // 128-byte row segment of tile rows xw * BM / 4 + lane with one 4-byte LDS-DMA load into a dummy
-  // LDS area (never read), so that the segment is in L2 by the time the real DMA of that step is
-  // issued, one step later. A load into a register would do the same, but the compiler would wait
-  // for it as soon as the register is reused.
+  // L2 prefetch of the gathered activation rows two steps ahead (MoE ping-pong DMA waves): DMA wave
+  // xw touches the 128-byte row segment of tile rows xw * BM / 4 + lane with one 4-byte LDS-DMA
+  // load, so that the segment is in L2 by the time the real DMA of that step is issued, one step
+  // later. The LDS target is st.x[2], which is null with two activation stages: an address outside
+  // the workgroup's LDS allocation, where the LDS discards the written data, so the load has no
+  // effect but the fetch. (A real 256-byte LDS target made the step 1.5% slower, and a load into a
+  // register folded into a sink a step later 3.7% slower through the extra registers it holds.)
   constexpr bool XPF = PP && MOE && QG_XPREFETCH;   // dense rows are contiguous: no gain measured there
   uint32_t pfoff = kOOB;
   if constexpr (XPF) {
@@ -409,12 +419,13 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   uint4 wv[kWD][WC];
   uint32_t sv[kWD][WC];
 
-  auto issue_w = [&](int kt_local, uint4 (&w)[WC], uint32_t (&s)[WC], int cnt) {
+  auto issue_w = [&](int kt_local, uint4 (&w)[WC], uint32_t (&s)[WC], int cnt, int i0 = 0) {
     const int kt = ks0 + kt_local;
     const bool live = kt_local < nk;
 #pragma unroll
     for (int i = 0; i < WC; ++i) {
       if (i >= cnt) break;
+      if (i < i0) continue;
       const uint32_t wo = live ? woff[i] + (uint32_t)kt * KT::kWStepBytes : kOOB;
       const uint32_t so = live ? soff[i] + (uint32_t)kt * 4u : kOOB;
       w[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wr, wo, 0, 0));
@@ -665,10 +676,24 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       constexpr int wset_issue = S % kWD, wset_next = (S + 1) % kWD;
       mfma_phase(xs_cur, ws_cur, false);                   // stage kt complete since the last barrier
       __builtin_amdgcn_s_barrier();
-      issue_w(kt + kWD, wv[wset_issue], sv[wset_issue], CQ);  // the set of step kt, dequantised last step
+      if constexpr (kVmemSplit > 0) {
+        // weight loads chunk by chunk, each followed by the dequantisation of one chunk of the
+        // other register set (the set of step kt, dequantised last step, receives step kt+kWD)
 #pragma unroll
-      for (int u = 0; u < CQ * kUnitsPerChunk; ++u)
-        dequant_unit(kt + 1, u, wv[wset_next], sv[wset_next], ws_cur ^ 1);
+        for (int i = 0; i < CQ; ++i) {
+          issue_w(kt + kWD, wv[wset_issue], sv[wset_issue], i + 1, i);
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int u = i * kUnitsPerChunk; u < (i + 1) * kUnitsPerChunk; ++u)
+            dequant_unit(kt + 1, u, wv[wset_next], sv[wset_next], ws_cur ^ 1);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else {
+        issue_w(kt + kWD, wv[wset_issue], sv[wset_issue], CQ);  // the set of step kt, dequantised last step
+#pragma unroll
+        for (int u = 0; u < CQ * kUnitsPerChunk; ++u)
+          dequant_unit(kt + 1, u, wv[wset_next], sv[wset_next], ws_cur ^ 1);
+      }
       wait_lgkm0();
       __builtin_amdgcn_s_barrier();
     };
@@ -676,17 +701,36 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       constexpr int S = decltype(S_)::value;
       constexpr int xs_cur = S % 2, xs_next = (S + 1) % 2, ws_cur = S & 1;
       constexpr int wset_issue = S % kWD, wset_next = (S + 1) % kWD;
-      issue_x(kt + 1, xs_next);                            // stage last read in step kt-1
-      __builtin_amdgcn_sched_barrier(0);                   // the wait below counts the loads after the DMA
-      issue_w(kt + kWD, wv[wset_issue], sv[wset_issue], CD);
-      __builtin_amdgcn_sched_barrier(0);
-      if constexpr (XPF) {
-        prefetch_x(kt + 2);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+      constexpr int NU = CD * kUnitsPerChunk;              // dequantisation units of this wave
+      // The activation DMA (stage last read in step kt-1) goes out in kVmemSplit groups with a
+      // share of the dequantisation after each, so the wave works while its loads queue in the
+      // address unit. The vector-memory order is unchanged: all DMA groups, then the weight
+      // loads, then the prefetch (the wait at the end of the step counts the loads after the DMA).
+      constexpr int G = kVmemSplit > 0 ? kVmemSplit : 1;
 #pragma unroll
-      for (int u = 0; u < CD * kUnitsPerChunk; ++u)
-        dequant_unit(kt + 1, u, wv[wset_next], sv[wset_next], ws_cur ^ 1);
+      for (int g = 0; g < G; ++g) {
+        issue_x(kt + 1, xs_next, g * XL / G, (g + 1) * XL / G);
+        __builtin_amdgcn_sched_barrier(0);
+        if (g == G - 1) {
+          issue_w(kt + kWD, wv[wset_issue], sv[wset_issue], CD);
+          __builtin_amdgcn_sched_barrier(0);
+          if constexpr (XPF) {
+            prefetch_x(kt + 2);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+        if constexpr (kVmemSplit > 0) {
+#pragma unroll
+          for (int u = g * NU / G; u < (g + 1) * NU / G; ++u)
+            dequant_unit(kt + 1, u, wv[wset_next], sv[wset_next], ws_cur ^ 1);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      if constexpr (kVmemSplit == 0) {
+#pragma unroll
+        for (int u = 0; u < NU; ++u)
+          dequant_unit(kt + 1, u, wv[wset_next], sv[wset_next], ws_cur ^ 1);
+      }
       load_frags(xs_cur, ws_cur, 0, 0);                    // prefetch for the MFMA phase
       __builtin_amdgcn_s_barrier();
       mfma_phase(xs_cur, ws_cur, true);
