@@ -137,10 +137,13 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ y
 }
 
 // out[t][n] = sum_j w[t*topk+j] * y2[t*topk+j][n], fp32 fused multiply-add in increasing j.
-// Each thread produces V (4 or 8) consecutive outputs of one token row, keeping V/4 * topk
-// independent 16-byte loads in flight; y2 is read exactly once, so its loads and the output
-// stores are non-temporal.
-template <int V, int KFIX>
+// Each thread produces V (4 or 8) outputs of one token row as V/4 groups of 4 consecutive ones,
+// keeping V/4 * topk independent 16-byte loads in flight. With SPREAD thread i of the row takes
+// 4-float chunks i, i + N/V, ..., so every wave-wide load or store covers 1 KiB of contiguous
+// memory (faster when y2 is still in the last-level cache); otherwise its V outputs are
+// consecutive (faster when y2 streams from HBM). y2 is read exactly once, so its loads and the
+// output stores are non-temporal.
+template <int V, int KFIX, bool SPREAD>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ y2, const float* __restrict__ w,
                                                       float* __restrict__ out, long groups, int topk_rt, int N) {
   static_assert(V == 4 || V == 8, "4 or 8 outputs per thread");
@@ -151,7 +154,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   if (gid >= groups) return;
   const int per_row = N / V;
   const long t = gid / per_row;
-  const int n0 = (int)(gid - t * per_row) * V;
+  const int i = (int)(gid - t * per_row);
+  int ncol[G];   // first column of each group of 4
+#pragma unroll
+  for (int g = 0; g < G; ++g) ncol[g] = SPREAD ? 4 * (i + g * per_row) : V * i + 4 * g;
   f32x4 acc[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -163,9 +169,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     for (int j = 0; j < KFIX; ++j) {
       const long a = t * KFIX + j;
       wj[j] = w[a];
-      const f32x4* src = reinterpret_cast<const f32x4*>(y2 + a * N + n0);
 #pragma unroll
-      for (int g = 0; g < G; ++g) v[j][g] = __builtin_nontemporal_load(src + g);
+      for (int g = 0; g < G; ++g) v[j][g] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(y2 + a * N + ncol[g]));
     }
 #pragma unroll
     for (int j = 0; j < KFIX; ++j)
@@ -177,18 +182,16 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     for (int j = 0; j < topk; ++j) {
       const long a = t * topk + j;
       const float wj = w[a];
-      const f32x4* src = reinterpret_cast<const f32x4*>(y2 + a * N + n0);
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        const f32x4 v = __builtin_nontemporal_load(src + g);
+        const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(y2 + a * N + ncol[g]));
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[g][c] = __builtin_fmaf(wj, v[c], acc[g][c]);
       }
     }
   }
-  f32x4* dst = reinterpret_cast<f32x4*>(out + t * N + n0);
 #pragma unroll
-  for (int g = 0; g < G; ++g) __builtin_nontemporal_store(acc[g], dst + g);
+  for (int g = 0; g < G; ++g) __builtin_nontemporal_store(acc[g], reinterpret_cast<f32x4*>(out + t * N + ncol[g]));
 }
 
 // y[i] = sum_{s < splits} ws[s][i], summed in increasing s (deterministic); 4 floats per thread.

@@ -126,6 +126,28 @@ def test_inconsistent_routing_is_reported(monkeypatch):
     q().moe(xd, dev_i32(torch, idx), dev_i32(torch, r.expert_offsets), wq, sc, 1, synth.FMT_Q8)
 
 
+@pytest.mark.parametrize("T", [1024, 3200])
+def test_combine_bitexact_both_mappings(T):
+    """The combine picks its column mapping by the size of y2 (at most 192 MiB: wave-contiguous
+    chunks; above: consecutive outputs per thread). T=1024 (64 MiB) and T=3200 (200 MiB), top-8,
+    N=2048: sampled tokens equal the host's fp32 FMA in increasing slot order, bit for bit."""
+    torch = torch_or_skip()
+    topk, N = 8, 2048
+    rng = synth.rng_for(41, T)
+    y2 = rng.standard_normal((T * topk, N), dtype=np.float32)
+    w = rng.uniform(0.01, 1.0, T * topk).astype(np.float32)
+    out = q().moe_combine(dev_f32(torch, y2), dev_f32(torch, w), topk)
+    torch.cuda.synchronize()
+    toks = np.unique(np.concatenate([rng.integers(0, T, 48), [0, T - 1]]))
+    got = out[torch.from_numpy(toks).cuda()].cpu().numpy()
+    exp = np.zeros((len(toks), N), np.float32)
+    for j in range(topk):
+        rows = toks * topk + j
+        exp = (w[rows, None].astype(np.float64) * y2[rows].astype(np.float64) + exp.astype(np.float64)).astype(np.float32)
+    print(f"[parity] combine T={T} ({T * topk * N * 4 / 2**20:.0f} MiB y2): {len(toks)} tokens compared bitwise", flush=True)
+    assert np.array_equal(got, exp)
+
+
 def test_swiglu_and_combine_small():
     torch = torch_or_skip()
     rng = synth.rng_for(8)
