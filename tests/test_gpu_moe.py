@@ -126,13 +126,14 @@ def test_inconsistent_routing_is_reported(monkeypatch):
     q().moe(xd, dev_i32(torch, idx), dev_i32(torch, r.expert_offsets), wq, sc, 1, synth.FMT_Q8)
 
 
-@pytest.mark.parametrize("T", [1024, 3200])
-def test_combine_bitexact_both_mappings(T):
+@pytest.mark.parametrize("T,topk", [(1024, 8), (3200, 8), (4200, 6)])
+def test_combine_bitexact_both_mappings(T, topk):
     """The combine picks its column mapping by the size of y2 (at most 192 MiB: wave-contiguous
-    chunks; above: consecutive outputs per thread). T=1024 (64 MiB) and T=3200 (200 MiB), top-8,
-    N=2048: sampled tokens equal the host's fp32 FMA in increasing slot order, bit for bit."""
+    chunks; above: consecutive outputs per thread). T=1024 top-8 (64 MiB), T=3200 top-8 (200 MiB)
+    and T=4200 top-6 (197 MiB, the kernel with a runtime slot count), N=2048: sampled tokens equal
+    the host's fp32 FMA in increasing slot order, bit for bit."""
     torch = torch_or_skip()
-    topk, N = 8, 2048
+    N = 2048
     rng = synth.rng_for(41, T)
     y2 = rng.standard_normal((T * topk, N), dtype=np.float32)
     w = rng.uniform(0.01, 1.0, T * topk).astype(np.float32)
