@@ -61,36 +61,6 @@ __device__ __forceinline__ int lds_chunk(int r, int c) {
   return r * kRowBytes + ((c ^ row_swizzle(r)) << 4);
 }
 
-// 16 int8 weights (one 16-byte load) -> 16 bf16 = w * s, as 8 packed dwords.
-__device__ __forceinline__ void dequant_q8x16(const uint4 w, float s, uint32_t out[8]) {
-  const uint32_t d[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float f0 = (float)(int8_t)(d[i]);
-    const float f1 = (float)(int8_t)(d[i] >> 8);
-    const float f2 = (float)(int8_t)(d[i] >> 16);
-    const float f3 = (float)(int8_t)(d[i] >> 24);
-    out[2 * i] = pack_bf16x2(f0 * s, f1 * s);
-    out[2 * i + 1] = pack_bf16x2(f2 * s, f3 * s);
-  }
-}
-
-// 32 packed nibbles (one 16-byte load, one scale block) -> 32 bf16 = (u - 8) * s,
-// element 2j from the low nibble of byte j, element 2j+1 from its high nibble.
-__device__ __forceinline__ void dequant_q4x32(const uint4 w, float s, uint32_t out[16]) {
-  const uint32_t d[4] = {w.x, w.y, w.z, w.w};
-  const float o = -8.0f * s;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const float lo = (float)((d[i] >> (8 * b)) & 0xFu);
-      const float hi = (float)((d[i] >> (8 * b + 4)) & 0xFu);
-      out[4 * i + b] = pack_bf16x2(__builtin_fmaf(lo, s, o), __builtin_fmaf(hi, s, o));
-    }
-  }
-}
-
 // h = silu(g) * u in fp32 (the SiLU-gated activation); shared by the fused epilogue and the
 // standalone kernel so both round the same fp32 value to bf16.
 // silu(g) = g / (1 + e^-g) with the hardware exponential and reciprocal (each within about one
@@ -270,7 +240,6 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   // weight LDS stage (two) all repeat
   constexpr int kPeriod = (XS == 3 || kWD == 3) ? 6 : (kWD == 4 ? 4 : 2);
   static_assert(kUnits % 4 == 0, "units must spread evenly over the four K16 sub-steps");
-  constexpr int kUnitsPerKK = kUnits / 4;
   constexpr int kMfmaPerKK = KT::kTM * KT::kTN;
   constexpr int kValuPerUnit = (FMT == kQ8) ? 20 : 22;
 
