@@ -10,7 +10,7 @@
 // wave w takes every WAVES-th chunk of that range, w first. A chunk is the 64 bytes of a weight
 // row that one lane group of a load instruction covers: 64 K elements for Q8 (lane group g
 // loads elements 16g..16g+15) and 128 for Q4 (lane group g loads the 32-element block g). A wave
-// keeps kSmDepth chunks in flight and issues the next chunk's loads as soon as it has dequantised
+// keeps kSmDepth<FMT> chunks in flight and issues the next chunk's loads as soon as it has dequantised
 // one: with every chunk issued up front, the memory system would return the chunks of all
 // waves in no particular order, leaving many waves idle until late and piling the
 // dequantisation up at the end.
@@ -29,7 +29,11 @@ namespace qg {
 constexpr int kSmRows = 32;       // weight rows per workgroup: two 16-row MFMA groups per wave
 constexpr int kSmMaxM = 16;       // activation rows = MFMA B columns
 constexpr int kSmWaves = 8;       // waves per workgroup
-constexpr int kSmDepth = 2;       // chunks of a wave in flight
+// chunks of a wave in flight: three for Q8, two for Q4, whose four dequantisation units per
+// load make the VALU work of a chunk twice as long (measured on MI355X at M = 1, 4, 16: Q8 three
+// 0-5% faster than two, Q4 three 8-15% slower; four, or 16 waves of two chunks, slower for both)
+template <int FMT>
+constexpr int kSmDepth = (FMT == kQ8) ? 3 : 2;
 
 struct SmallArgs {
   const uint16_t* x;      // bf16 [M][K]
@@ -126,7 +130,7 @@ __global__ __launch_bounds__(WAVES * 64) void smallm_kernel(SmallArgs a) {
     for (int u = 0; u < U; ++u)
       xv[j][u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xok ? xo + 16u * u : kOOB, 0, 0));
   };
-  constexpr int D = JW < kSmDepth ? JW : kSmDepth;
+  constexpr int D = JW < kSmDepth<FMT> ? JW : kSmDepth<FMT>;
 #pragma unroll
   for (int j = 0; j < D; ++j) issue(j);
   __builtin_amdgcn_sched_barrier(0);   // keep these loads ahead of the first LDS write
