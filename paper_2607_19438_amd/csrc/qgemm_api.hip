@@ -206,11 +206,16 @@ int launch_moe_cfg(qg::TileArgs a, const void* const* wq, const void* const* sc,
   return QGEMM_OK;
 }
 
-// Tile height from the mean rows per expert (the host does not see the routing): groups of
-// about 100-200 rows fit one 192-row tile each; larger groups use 256-row tiles.
+// Tile from the mean rows per expert (the host does not see the routing): groups of about
+// 100-200 rows fit one 192-row tile each; larger groups use 256-row tiles. Short prompts (at
+// most 32 rows per expert on average) use 128x128 tiles of four waves, two workgroups per CU:
+// twice the workgroups of the 256-wide tiles over the few active experts' weights, so the
+// CUs fill (measured at T=128, E=128, top-8: gate/up + SiLU 66.5 against 73 us, down 31
+// against 34 us; at T=2048 the same tile is slower, 196 against 159 us and 125 against 108 us).
 template <int FMT, bool SWI = false>
 int launch_moe(qg::TileArgs a, const void* const* wq, const void* const* sc, int E, hipStream_t s) {
   const long mean_rows = (long)a.M / E;
+  if (mean_rows <= 32) return launch_moe_cfg<FMT, 128, 128, 2, 2, 2, SWI>(a, wq, sc, E, s);
   if (mean_rows > 192) return launch_moe_cfg<FMT, 256, 256, 2, 4, 2, SWI>(a, wq, sc, E, s);
   return launch_moe_cfg<FMT, 192, 256, 2, 4, 2, SWI>(a, wq, sc, E, s);
 }

@@ -918,7 +918,8 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
 // workgroup decodes its item from the per-expert counts, so the host never
 // needs the routing.
 template <int FMT, int BM, int BN, int WM, int WN, int XS, bool SWI>
-__global__ __launch_bounds__(WM * WN * 64) void moe_kernel(TileArgs a, ExpertPtrs ep) {
+// four-wave tiles (67 KB of LDS) run two workgroups per CU: at most 256 registers per lane
+__global__ __launch_bounds__(WM * WN * 64, WM * WN == 4 ? 2 : 1) void moe_kernel(TileArgs a, ExpertPtrs ep) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, true, XS>;
   static_assert(KT::kThreads >= kMaxExpertsPerLaunch, "the tile prefix needs one lane per expert");
   __shared__ __attribute__((aligned(1024))) char lx0[KT::kXTileBytes];
