@@ -160,3 +160,39 @@ def test_small_groups_write_only_their_rows():
     b = big.cpu().numpy()
     assert np.all(b[:pad] == 7.5) and np.all(b[pad + A:] == 7.5)
     check("moe_fewrows guard", x, r, ws, fmt, y.cpu().numpy(), 256)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_tile_choice_boundary_bitwise(fmt):
+    """At most 32 rows per expert on average a launch takes 128x128 four-wave tiles, above that
+    192x256 eight-wave tiles. Both add the same MFMA products in the same K order, so a row routed
+    identically in a launch just below and one just above the boundary is bitwise equal; each
+    launch also meets the oracle's bar. Plain grouped GEMM and the fused gate/up + SiLU epilogue."""
+    torch = torch_or_skip()
+    m = q()
+    K, inter = 512, 128
+    counts = [32, 40, 20, 36]                       # 128 rows over 4 experts: mean 32
+    rng = synth.rng_for(28, fmt, *counts)
+    idx_a = np.repeat(np.arange(len(counts), dtype=np.int32), counts)
+    rng.shuffle(idx_a)
+    idx_b = np.concatenate([idx_a, np.zeros(4, np.int32)])   # 132 rows: mean 33
+    x_b = synth.make_x(rng, idx_b.size, K)
+    x_a = np.ascontiguousarray(x_b[:idx_a.size])
+    ws = [synth.make_qweight(rng, 2 * inter, K, fmt) for _ in counts]
+    wq, sc = dev_experts(torch, ws)
+    table = m.ExpertTable(wq, sc, fmt)
+    ys, hs = [], []
+    for x, idx in ((x_a, idx_a), (x_b, idx_b)):
+        r = synth.routing_from_idx(idx, len(counts), 1, np.ones(idx.size, np.float32))
+        off = dev_i32(torch, r.expert_offsets)
+        perm = m.moe_bucket(dev_i32(torch, r.token_expert_idx), off)
+        y = m.moe_grouped(dev_x(torch, x), perm, off, table, None, 1, fmt)
+        h = m.moe_gate_up_swiglu(dev_x(torch, x), perm, off, table, None, 1, fmt)
+        torch.cuda.synchronize()
+        y = y.cpu().numpy()
+        check(f"moe tile boundary rows={idx.size} {synth.FMT_NAMES[fmt]}", x, r, ws, fmt, y, K)
+        ys.append(y)
+        hs.append(h.cpu().view(torch.int16).numpy().view(np.uint16))
+    n = idx_a.size
+    assert np.array_equal(ys[0].view(np.uint32), ys[1][:n].view(np.uint32))
+    assert np.array_equal(hs[0], hs[1][:n])
