@@ -24,6 +24,10 @@ FFN at a 128-token prompt, the HBM-bound tail of the MoE path, weights read from
 against the HBM roofline) and ``attention`` (prefill flash attention of a 2048-token
 prompt, 32 query / 4 key-value heads, D=128, causal, against the bf16 MFMA peak).
 
+Before the counted warmup the step is repeated in 5-step groups until at least --prewarm-min-s
+seconds have run and two consecutive group means agree within 2% (the GPU clock ramps up over the
+first ~25 steps after start-up), so a small --warmup still times the warm step.
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        [--small-m-launches L] [--attention-launches L] [--moe-t128-launches L]
        [--small-m-only] [--attention-only] [--moe-t128-only]
@@ -51,8 +55,18 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=30,
-                    help="untimed steps; the first ~25 steps after start-up run slower (clock ramp)")
+    ap.add_argument("--warmup", type=int, default=5,
+                    help="untimed steps after the prewarm")
+    ap.add_argument("--prewarm-min-s", type=float, default=1.0,
+                    help="before the counted warmup, repeat 5-step groups until at least this much time has run "
+                         "and two consecutive group means agree within --prewarm-tol (the clock ramps up over the "
+                         "first ~25 steps after start-up)")
+    ap.add_argument("--prewarm-tol", type=float, default=0.02)
+    ap.add_argument("--prewarm-max-s", type=float, default=20.0)
+    ap.add_argument("--dense-config-launches", type=int, default=100,
+                    help="launches per case of the dense Q8 M=128 and dense Q4 M=512 workloads (0: skip)")
+    ap.add_argument("--clock-probe-iters", type=int, default=400000,
+                    help="MFMA rounds per wave of the clock probe (~50 ms; 0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seconds", type=float, default=15.0)
     ap.add_argument("--no-events", action="store_true",
@@ -73,6 +87,8 @@ def parse():
                     help="run only the prefill-attention section and print its JSON")
     ap.add_argument("--small-m-only", action="store_true",
                     help="run only the small-M section and print its JSON (for kernel traces of those cases)")
+    ap.add_argument("--dense-configs-only", action="store_true",
+                    help="run only the dense M=128 / M=512 workload section and print its JSON")
     return ap.parse_args()
 
 
@@ -253,6 +269,89 @@ def small_m_section(torch, q, synth, launches):
             "cases": rows}
 
 
+def dense_configs_section(torch, q, synth, launches):
+    """The two dense workloads outside the step: Q8 M=128 x K=1024 x N=1024 (latency / HBM bound) and
+    Q4 M=512 x K=3072 x N=8192 (MFMA bound), each timed two ways: weight copies rotated over ~1 GiB so
+    every launch reads its weights from HBM, and one weight set reused (last-level-cache resident)."""
+    dev = torch.device("cuda:0")
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    a, b = ev(), ev()
+    a.record()
+    torch.cuda._sleep(1 << 22)
+    b.record()
+    torch.cuda.synchronize()
+    ms_per_cycle = a.elapsed_time(b) / (1 << 22)
+    out = {}
+    for cfg in (0, 1):
+        (case,) = synth.config(cfg)
+        wq0 = torch.from_numpy(case.w.wq).to(dev)
+        sc0 = torch.from_numpy(case.w.scales).to(dev)
+        wbytes = wq0.numel() + 2 * sc0.numel()
+        R = max(2, -(-ROTATE_BYTES // wbytes))
+        copies = [(wq0.clone(), sc0.clone()) for _ in range(R)]
+        x = torch.from_numpy(np.ascontiguousarray(case.x).view(np.int16)).view(torch.bfloat16).to(dev)
+        y = torch.empty((case.M, case.N), dtype=torch.float32, device=dev)
+        for wq, sc in copies:
+            q.dense(x, wq, sc, case.fmt, out=y)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(20):
+            q.dense(x, *copies[i % R], case.fmt, out=y)
+        host_us = (time.perf_counter() - t0) / 20 * 1e6
+        torch.cuda.synchronize()
+        res = {"workload": case.name, "M": case.M, "N": case.N, "K": case.K, "fmt": "q8" if case.fmt == 0 else "q4",
+               "flop_per_launch": case.flops}
+        for mode in ("hbm", "cached"):
+            first, last = ev(), ev()
+            torch.cuda._sleep(int(3 * launches * host_us * 1e-3 / ms_per_cycle))
+            first.record()
+            for i in range(launches):
+                q.dense(x, *(copies[i % R] if mode == "hbm" else copies[0]), case.fmt, out=y)
+            last.record()
+            torch.cuda.synchronize()
+            us = first.elapsed_time(last) / launches * 1e3
+            nbytes = wbytes + 2 * case.M * case.K + 4 * case.M * case.N
+            tf = case.flops / (us * 1e-6) / 1e12
+            res[mode] = {"us_per_launch": us, "TFLOP/s": tf, "frac_mfma": tf / PEAK_BF16_TFLOPS,
+                         "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_hbm": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+                         "bytes_per_launch": nbytes}
+            log(f"{case.name} ({mode}): {us:.2f} us/launch, {tf:.0f} TFLOP/s, {res[mode]['GB/s']:.0f} GB/s")
+        res["weight_copies_rotated"] = R
+        res["launches"] = launches
+        # the roofline that bounds each workload (algorithmic work: bytes of x + packed weights + y)
+        res["bound"] = "mfma" if case.flops / res["hbm"]["bytes_per_launch"] > PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3 else "hbm"
+        out[f"cfg{cfg}"] = res
+        del copies, wq0, sc0
+        torch.cuda.empty_cache()
+    return out
+
+
+def prewarm(torch, q, parts, min_s, tol, max_s):
+    """Run 5-step groups until at least `min_s` seconds have passed and two consecutive group means
+    agree within `tol` (or `max_s` is reached): the clock ramps up over the first steps after start-up."""
+    plain = EventTimer(torch, False)
+    means = []
+    steps = 0
+    t_start = time.perf_counter()
+    while True:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(5):
+            for p in parts:
+                run_part(q, p, plain)
+        torch.cuda.synchronize()
+        means.append((time.perf_counter() - t0) / 5 * 1e3)
+        steps += 5
+        spent = time.perf_counter() - t_start
+        stable = len(means) >= 2 and abs(means[-1] - means[-2]) <= tol * means[-2]
+        if (spent >= min_s and stable) or spent >= max_s:
+            break
+    log(f"prewarm: {steps} steps in {spent:.2f} s; 5-step means (ms/step) first {means[0]:.3f}, "
+        f"last two {means[-2] if len(means) > 1 else float('nan'):.3f} / {means[-1]:.3f}")
+    return {"prewarm_steps": steps, "prewarm_s": spent, "stable": bool(stable),
+            "group_ms_per_step_first": means[0], "group_ms_per_step_last": means[-1]}
+
+
 # The skewed MoE FFN of the T=8192 workload at a 128-token prompt: 1024 token slots over the
 # active experts only, so every projection reads each active expert's packed weights about once
 # for a few rows -- the HBM-bound tail of the MoE path. Reported beside the step, not part of
@@ -407,8 +506,32 @@ def cpu_baseline(synth, seconds):
         T_s *= 2
         if spent + 2.2 * dt > 2 * seconds:
             break
+    # one single-thread figure: the whole dense Q8 M=128 workload (0.27 GFLOP)
+    (c0,) = synth.config(0)
+    single = None
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1, user_api="blas"):
+            t0 = time.perf_counter()
+            oracle.dense(c0.x, c0.w.wq, c0.w.scales, c0.fmt)
+            dt1 = time.perf_counter() - t0
+        single = {"workload": c0.name, "seconds": dt1, "GFLOP/s": c0.flops / dt1 / 1e9, "threads": 1}
+    except Exception as exc:  # pragma: no cover - threadpoolctl missing
+        log(f"single-thread oracle timing skipped: {exc}")
     return {"value": flops / spent / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "cpu_model": cpu_model(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "single_thread_cfg0": single,
             "sample": "; ".join(done) + f" ({spent:.1f} s of fp64 CPU work; FLOP counted as 2*M*N*K of the sampled rows)"}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def main():
@@ -444,11 +567,15 @@ def main():
     if args.moe_t128_only:
         print(json.dumps({"moe_t128": moe_t128_section(torch, q, synth, args.moe_t128_launches)}), flush=True)
         return 0
+    if args.dense_configs_only:
+        print(json.dumps(dense_configs_section(torch, q, synth, args.dense_config_launches)), flush=True)
+        return 0
     log("generating inputs")
     t0 = time.perf_counter()
     parts = build_parts(torch, q, synth, args.only, fused=not args.unfused)
     torch.cuda.synchronize()
     log(f"inputs resident in HBM ({time.perf_counter() - t0:.1f} s)")
+    pre = prewarm(torch, q, parts, args.prewarm_min_s, args.prewarm_tol, args.prewarm_max_s)
     plain = EventTimer(torch, False)
     for _ in range(args.warmup):
         for p in parts:
@@ -466,6 +593,7 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     log(f"timed {args.steps} steps in {wall:.3f} s (host enqueue {enq / args.steps * 1e3:.3f} ms/step)")
+    host_enqueue_ms = enq / args.steps * 1e3
     ms_per_step = wall / args.steps * 1e3
     flops_step = sum(p.flops for p in parts)
     value = flops_step / (wall / args.steps) / 1e12
@@ -500,6 +628,19 @@ def main():
                 "launch_ms": per[dom], "flop_per_launch": flops_of[dom]}
     log(f"instrumented pass: {wall_ev / args.steps * 1e3:.3f} ms/step")
 
+    clock = None
+    if args.clock_probe_iters > 0:
+        clock = q.probe_mfma_clock(args.clock_probe_iters)
+        clock["mfma_probe_frac_of_peak"] = clock["mfma_tflops"] / PEAK_BF16_TFLOPS
+        clock["iters"] = args.clock_probe_iters
+        log(f"clock under full MFMA load: {clock['sclk_mhz']:.0f} MHz; MFMA-only probe "
+            f"{clock['mfma_tflops']:.0f} TFLOP/s ({clock['mfma_probe_frac_of_peak']:.3f} of the 2.4 GHz peak)")
+
+    dense_cfgs = None
+    if args.dense_config_launches > 0 and not args.only:
+        log("dense workloads Q8 M=128 and Q4 M=512")
+        dense_cfgs = dense_configs_section(torch, q, synth, args.dense_config_launches)
+
     small = None
     if args.small_m_launches > 0 and not args.only:
         log("small-M (decode / verification) cases")
@@ -531,6 +672,11 @@ def main():
                    "frac_of_mfma_peak": value / PEAK_BF16_TFLOPS, "flop_per_step": flops_step},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "prewarm": pre,
+        "host_enqueue_ms_per_step": host_enqueue_ms,
+        "instrumented_ms_per_step": wall_ev / args.steps * 1e3,
+        "clock": clock,
+        "dense_configs": dense_cfgs,
         "breakdown": breakdown,
         "small_m": small,
         "attention": attn,

@@ -71,7 +71,7 @@ enum qgemm_status {
  * library-owned workspace (grown on first use, freed by qgemm_release);
  * concurrent calls on different streams must not share it.
  * M <= 16 (decode and speculative-draft verification, the memory-bound
- * regime of Section 4.1 and the batched verification of Section 6) takes a
+ * regime of Section 2.3 and the batched verification of Section 5.2) takes a
  * separate bandwidth-oriented kernel: weights dequantised straight into
  * matrix-core registers, K split over waves (and over workgroups when N is
  * small, through the same workspace); its results are bitwise reproducible
@@ -189,6 +189,18 @@ const char* qgemm_last_error(void);
 int qgemm_attention_prefill(const void* q, const void* k, const void* v, void* o,
                             int B, int S, int H, int Hkv, int D,
                             float scale, int causal, hipStream_t stream);
+
+/*
+ * Measurement utility, not part of the GEMM path: runs `iters` rounds of four
+ * independent bf16 MFMAs (the GEMM's v_mfma_f32_32x32x16_bf16) in eight waves on
+ * every CU at once, synchronises `stream`, and returns through HOST pointers
+ * the median shader clock the CUs held (MHz; cycle counter over the device's
+ * constant-rate real-time counter) and the bf16 dense matrix throughput the
+ * launch reached (TFLOP/s, from HIP events on `stream`): the practical matrix-core
+ * ceiling at the sustained clock, beside the nominal 2.4 GHz peak. Allocates and
+ * frees its own small buffers. QGEMM_EINVAL for iters < 1 or null outputs.
+ */
+int qgemm_probe_mfma_clock(int iters, double* sclk_mhz, double* mfma_tflops, hipStream_t stream);
 
 /* Frees the library-owned workspaces (MoE bucketing, split-K partials); the
  * next call that needs one grows it again. The caller must have synchronised

@@ -16,7 +16,7 @@ import os
 import torch  # imported before the library so that both share one HIP runtime
 
 __all__ = ["Q8", "Q4", "QGemmError", "lib", "lib_path", "dense", "moe", "moe_bucket", "moe_grouped",
-           "moe_gate_up_swiglu", "swiglu", "moe_combine", "attention_prefill", "last_error", "release", "version", "EXPORTS", "ExpertTable"]
+           "moe_gate_up_swiglu", "swiglu", "moe_combine", "attention_prefill", "probe_mfma_clock", "last_error", "release", "version", "EXPORTS", "ExpertTable"]
 
 Q8 = 0
 Q4 = 1
@@ -35,6 +35,7 @@ EXPORTS = {
     "qgemm_swiglu": (_i, [_vp, _vp, _i, _i, _vp]),
     "qgemm_moe_combine": (_i, [_vp, _vp, _vp, _i, _i, _i, _vp]),
     "qgemm_attention_prefill": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, ctypes.c_float, _i, _vp]),
+    "qgemm_probe_mfma_clock": (_i, [_i, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), _vp]),
     "qgemm_last_error": (ctypes.c_char_p, []),
     "qgemm_release": (_i, []),
     "qgemm_version": (_i, []),
@@ -302,3 +303,13 @@ def attention_prefill(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal:
     _check(lib().qgemm_attention_prefill(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), B, S, H, Hkv, D,
                                          float(scale), int(bool(causal)), _stream(q)))
     return out
+
+
+def probe_mfma_clock(iters: int = 100000):
+    """Sustained shader clock (MHz) and bf16 MFMA throughput (TFLOP/s) under full matrix-core load
+    (``qgemm_probe_mfma_clock``; synchronises the current stream). A measurement utility."""
+    mhz = ctypes.c_double(0.0)
+    tf = ctypes.c_double(0.0)
+    _check(lib().qgemm_probe_mfma_clock(int(iters), ctypes.byref(mhz), ctypes.byref(tf),
+                                        torch.cuda.current_stream().cuda_stream))
+    return {"sclk_mhz": mhz.value, "mfma_tflops": tf.value}

@@ -570,6 +570,57 @@ int qgemm_attention_prefill(const void* q, const void* k, const void* v, void* o
   return rc == QGEMM_OK ? ok() : rc;
 }
 
+int qgemm_probe_mfma_clock(int iters, double* sclk_mhz, double* mfma_tflops, hipStream_t stream) {
+  if (iters < 1 || !sclk_mhz || !mfma_tflops) return fail(QGEMM_EINVAL, "iters must be >= 1 and outputs non-null");
+  int dev = 0, ncu = 0, rt_khz = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipDeviceGetAttribute(&rt_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || ncu < 1 || rt_khz < 1) {
+    (void)hipGetLastError();
+    return fail(QGEMM_EHIP, "device attribute query failed");
+  }
+  long long* stamps = nullptr;
+  float* sink = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = QGEMM_OK;
+  if (hipMalloc(reinterpret_cast<void**>(&stamps), (size_t)ncu * 4 * sizeof(long long)) != hipSuccess ||
+      hipMalloc(reinterpret_cast<void**>(&sink), qg::kProbeThreads * sizeof(float)) != hipSuccess ||
+      hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+    rc = fail(QGEMM_EHIP, "probe set-up failed");
+  }
+  std::vector<long long> h((size_t)ncu * 4);
+  float ms = 0.0f;
+  if (rc == QGEMM_OK) {
+    (void)hipGetLastError();
+    (void)hipEventRecord(e0, stream);
+    hipLaunchKernelGGL(qg::mfma_clock_probe_kernel, dim3(ncu), dim3(qg::kProbeThreads), 0, stream, stamps, iters, sink);
+    rc = check_launch("qgemm_probe_mfma_clock");
+    (void)hipEventRecord(e1, stream);
+    if (rc == QGEMM_OK) {
+      if (hipStreamSynchronize(stream) != hipSuccess || hipEventElapsedTime(&ms, e0, e1) != hipSuccess ||
+          hipMemcpy(h.data(), stamps, h.size() * sizeof(long long), hipMemcpyDeviceToHost) != hipSuccess)
+        rc = fail(QGEMM_EHIP, "probe read-back failed");
+    }
+  }
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (stamps) (void)hipFree(stamps);
+  if (sink) (void)hipFree(sink);
+  (void)hipGetLastError();
+  if (rc != QGEMM_OK) return rc;
+  std::vector<double> mhz;
+  for (int b = 0; b < ncu; ++b) {
+    const double dc = (double)(h[4 * b + 1] - h[4 * b]);
+    const double dt = (double)(h[4 * b + 3] - h[4 * b + 2]) / ((double)rt_khz * 1e3);   // seconds
+    if (dt > 0 && dc > 0) mhz.push_back(dc / dt * 1e-6);
+  }
+  if (mhz.empty() || !(ms > 0.0f)) return fail(QGEMM_EHIP, "probe produced no timing");
+  std::sort(mhz.begin(), mhz.end());
+  *sclk_mhz = mhz[mhz.size() / 2];
+  const double flop = (double)ncu * (qg::kProbeThreads / 64) * (double)iters * 4.0 * 32.0 * 32.0 * 16.0 * 2.0;
+  *mfma_tflops = flop / ((double)ms * 1e-3) / 1e12;
+  return ok();
+}
+
 int qgemm_release(void) {
   std::lock_guard<std::mutex> lock(g_ws_mutex);
   int cur = 0;

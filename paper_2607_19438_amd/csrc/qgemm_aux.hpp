@@ -211,3 +211,58 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 }
 
 }  // namespace qg
+
+namespace qg {
+
+// Measurement probe (not on the GEMM path): every wave issues `iters` rounds of four independent
+// bf16 MFMAs (v_mfma_f32_32x32x16_bf16, the GEMM's instruction) on register operands, so the
+// matrix cores run at their sustained rate. Wave 0 of each workgroup records the shader-clock
+// counter and the constant-rate real-time counter before and after; their ratio is the clock the
+// chip holds under full matrix-core load. out: [gridDim.x][4] int64 (clock start, clock end,
+// real-time start, real-time end); sink keeps the accumulators alive (written only if a lane's sum
+// is exactly 1234.5, which the operands never produce).
+constexpr int kProbeThreads = 512;
+__global__ __launch_bounds__(kProbeThreads) void mfma_clock_probe_kernel(long long* __restrict__ out, int iters,
+                                                                          float* __restrict__ sink) {
+  // 96 KiB of LDS: at most one workgroup per CU (160 KiB), so a grid of one workgroup per CU
+  // puts eight waves, two per SIMD, on every CU at once
+  __shared__ char probe_lds[96 * 1024];
+  typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+  typedef float f32x16_t __attribute__((ext_vector_type(16)));
+  const int lane = threadIdx.x & 63;
+  bf16x8_t a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(0.001f * (float)((lane + i) & 7));
+    b[i] = (__bf16)(0.002f * (float)((lane * 3 + i) & 7));
+  }
+  f32x16_t c0 = {}, c1 = {}, c2 = {}, c3 = {};
+  __syncthreads();
+  long long t0 = 0, r0 = 0;
+  if (threadIdx.x == 0) {
+    t0 = (long long)__builtin_readcyclecounter();
+    r0 = (long long)__builtin_amdgcn_s_memrealtime();
+  }
+  for (int it = 0; it < iters; ++it) {
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) s += c0[i] + c1[i] + c2[i] + c3[i];
+  if (s == 1234.5f) sink[threadIdx.x] = s + (float)probe_lds[threadIdx.x];
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const long long t1 = (long long)__builtin_readcyclecounter();
+    const long long r1 = (long long)__builtin_amdgcn_s_memrealtime();
+    long long* o = out + 4 * (long)blockIdx.x;
+    o[0] = t0;
+    o[1] = t1;
+    o[2] = r0;
+    o[3] = r1;
+  }
+}
+
+}  // namespace qg

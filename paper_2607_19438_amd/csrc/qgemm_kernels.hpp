@@ -194,7 +194,7 @@ typedef __attribute__((address_space(3))) char lds_char;
 // the compiler can tell they do not alias and keeps the DMA in flight across them instead of
 // draining it (vmcnt) before every LDS access.
 struct LdsStages {
-  char* x[3];   // activation stages; x[2] is null with two stages (see the activation prefetch)
+  char* x[3];   // activation stages; with two stages x[2] is a 256-byte sink (the activation prefetch)
   char* w[2];
 };
 
@@ -364,10 +364,9 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   // L2 prefetch of the gathered activation rows two steps ahead (MoE ping-pong DMA waves): DMA wave
   // xw touches the 128-byte row segment of tile rows xw * BM / 4 + lane with one 4-byte LDS-DMA
   // load, so that the segment is in L2 by the time the real DMA of that step is issued, one step
-  // later. The LDS target is st.x[2], which is null with two activation stages: an address outside
-  // the workgroup's LDS allocation, where the LDS discards the written data, so the load has no
-  // effect but the fetch. (A real 256-byte LDS target made the step 1.5% slower, and a load into a
-  // register folded into a sink a step later 3.7% slower through the extra registers it holds.)
+  // later. The LDS target is st.x[2], a 256-byte array no other access reads or writes (64 lanes
+  // x 4 bytes): every wave's prefetch overwrites it, so the load's only effect is the fetch. (A
+  // load into a register folded into a sink a step later was slower through the registers it holds.)
   constexpr bool XPF = PP && MOE && QG_XPREFETCH;   // dense rows are contiguous: no gain measured there
   uint32_t pfoff = kOOB;
   if constexpr (XPF) {
@@ -893,7 +892,7 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
   __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 256];
   __shared__ __attribute__((aligned(1024))) char lw0[KT::kWTileBytes];
   __shared__ __attribute__((aligned(1024))) char lw1[KT::kWTileBytes];
-  const LdsStages lds{{lx0, lx1, XS == 3 ? lx2 : nullptr}, {lw0, lw1}};
+  const LdsStages lds{{lx0, lx1, lx2}, {lw0, lw1}};
   const int mt_n = (a.M + BM - 1) / BM;
   const int nt_n = (a.N + BN - 1) / BN;
   const int ntiles = mt_n * nt_n;
@@ -927,7 +926,7 @@ __global__ __launch_bounds__(WM * WN * 64, WM * WN == 4 ? 2 : 1) void moe_kernel
   __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 256];
   __shared__ __attribute__((aligned(1024))) char lw0[KT::kWTileBytes];
   __shared__ __attribute__((aligned(1024))) char lw1[KT::kWTileBytes];
-  const LdsStages lds{{lx0, lx1, XS == 3 ? lx2 : nullptr}, {lw0, lw1}};
+  const LdsStages lds{{lx0, lx1, lx2}, {lw0, lw1}};
   __shared__ int s_prefix[kMaxExpertsPerLaunch + 1];
   __shared__ int s_rowidx[BM];   // y row (assignment) of each tile row
   __shared__ int s_xrow[BM];     // x row (token = assignment / topk) of each tile row

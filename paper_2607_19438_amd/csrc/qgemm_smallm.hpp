@@ -1,6 +1,6 @@
 // Small-M dense GEMM (at most 16 activation rows): the shape of decode and of batched
 // speculative-draft verification, which the paper names as the memory-bound side of inference
-// (Section 4.1) and as future work for its matrix-unit kernels (Section 6). Every packed weight
+// (Section 2.3) and as future work for its matrix-unit kernels (Section 5.2). Every packed weight
 // is read once and the arithmetic per weight byte is tiny, so the call is bound by HBM bandwidth:
 // there is no LDS staging of the weights. Each lane dequantises its own 16-byte weight load
 // straight into MFMA operand registers (v_mfma_f32_16x16x32_bf16, weights as the 16-row A

@@ -225,12 +225,17 @@ def check_moe_case(torch, case, n_tokens, n_samples, split=False):
 
 
 def check_chain(name, out, o_ref, o_b, o_tol):
-    """FFN output: within the tolerance that carries each GEMM's bar through SiLU and bf16 rounding."""
-    r_tol = float(np.max(np.abs(out - o_ref) / o_tol))
+    """FFN output against the oracle's own chain: the plain acceptance bar with the router-weighted
+    bound (|out - out_ref| <= 1e-3 * sum_j |w_j| sum_i |h_i W_down| + 1e-6), and, tighter in the
+    direction that matters for a wrong h, the tolerance that carries each GEMM's bar through SiLU
+    and the bf16 rounding of h."""
+    r_tol = float(np.max(np.abs(out - o_ref) / o_tol)) if np.isfinite(out).all() else float("inf")
     r_bar = oracle.bar_ratio(out, o_ref, o_b)
-    print(f"[parity] {name}: ratio to propagated tolerance = {r_tol:.3e} "
-          f"(plain 1e-3 bar ratio, informational: {r_bar:.3e})", flush=True)
-    assert np.isfinite(out).all() and r_tol <= 1.0
+    print(f"[parity] {name}: plain 1e-3 bar ratio = {r_bar:.3e}; ratio to propagated tolerance = {r_tol:.3e}",
+          flush=True)
+    assert np.isfinite(out).all()
+    assert r_bar <= 1.0, f"{name}: FFN output exceeds the acceptance bar ({r_bar})"
+    assert r_tol <= 1.0, f"{name}: FFN output exceeds the propagated tolerance ({r_tol})"
 
 
 @pytest.mark.parametrize("cfg,T", [(3, None), (4, None), (4, 128)])

@@ -247,3 +247,114 @@ def test_ffn_tolerance_covers_perturbed_chains(fmt):
         worst = max(worst, float(np.max(np.abs(outp - res["out"]) / tol)))
     assert worst <= 1.0
     assert worst > 0.05          # the tolerance is not vacuous
+
+
+# ---------------------------------------------------------------------------
+# moe_entries: the per-element MoE evaluation the full-size GPU checks sample
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_moe_entries_exact_rational(fmt):
+    """Every (assignment, column) of a tiny top-3 case against exact rational arithmetic:
+    row a reads token a // topk and the weights of expert idx[a] (not of another slot)."""
+    T, E, topk, N, K = 4, 5, 3, 3, 64
+    x, r, ws = small_moe(21, T=T, E=E, topk=topk, N=N, K=K, fmt=fmt)
+    A = T * topk
+    assigns = np.repeat(np.arange(A), N)
+    cols = np.tile(np.arange(N), A)
+    y, bound = oracle.moe_entries(x, r.token_expert_idx, [w.wq for w in ws], [w.scales for w in ws], topk, fmt,
+                                  assigns, cols)
+    for i, (a, n) in enumerate(zip(assigns, cols)):
+        t, e = int(a) // topk, int(r.token_expert_idx[a])
+        terms = [Fraction(bf16_value_struct(x[t, k])) * Fraction(float(ws[e].scales[n, k // 32])) * int(ws[e].q[n, k])
+                 for k in range(K)]
+        ex = sum(terms)
+        bx = sum(abs(v) for v in terms)
+        assert abs(Fraction(y[i]) - ex) <= K * 2.0 ** -52 * bx, (a, n)
+        assert abs(Fraction(bound[i]) - bx) <= K * 2.0 ** -52 * bx, (a, n)
+
+
+@pytest.mark.parametrize("bf16_weights", [False, True])
+@pytest.mark.parametrize("fmt", FMTS)
+def test_moe_entries_match_moe(fmt, bf16_weights):
+    """Sampled entries (random pairs, every corner, every row of one expert at the last column)
+    equal the expert-major oracle, with empty experts (NaN scales that must never be read)."""
+    T, E, topk, N, K = 23, 9, 3, 40, 96
+    x, r, ws = small_moe(22, T=T, E=E, topk=topk, N=N, K=K, fmt=fmt)
+    idx = r.token_expert_idx.copy()
+    idx[idx == 4] = 0                       # experts 4 and 7 receive nothing
+    idx[idx == 7] = 8
+    # keep each token's experts distinct (top-k never repeats an expert)
+    idx = idx.reshape(T, topk)
+    for t in range(T):
+        seen = set()
+        for j in range(topk):
+            while idx[t, j] in seen or idx[t, j] in (4, 7):
+                idx[t, j] = (idx[t, j] + 1) % E
+            seen.add(int(idx[t, j]))
+    idx = idx.reshape(-1)
+    rr = synth.routing_from_idx(idx, E, topk)
+    assert rr.counts[4] == 0 and rr.counts[7] == 0
+    ss = [w.scales.copy() for w in ws]
+    for e in (4, 7):
+        ss[e][:] = np.float16(np.nan)
+    wq = [w.wq for w in ws]
+    y, b = oracle.moe(x, idx, rr.expert_offsets, wq, ss, topk, fmt, bf16_weights=bf16_weights)
+    rng = synth.rng_for(23, fmt)
+    A = T * topk
+    rows = list(rng.integers(0, A, 300)) + [0, 0, A - 1, A - 1]
+    cols = list(rng.integers(0, N, 300)) + [0, N - 1, 0, N - 1]
+    for a in np.nonzero(idx == 0)[0]:
+        rows.append(int(a))
+        cols.append(N - 1)
+    rows, cols = np.array(rows), np.array(cols)
+    ye, be = oracle.moe_entries(x, idx, wq, ss, topk, fmt, rows, cols, bf16_weights=bf16_weights)
+    assert np.isfinite(ye).all()
+    np.testing.assert_allclose(ye, y[rows, cols], rtol=0, atol=K * 2.0 ** -52 * b.max())
+    np.testing.assert_allclose(be, b[rows, cols], rtol=1e-13)
+
+
+def test_moe_entries_bf16_weights_round_each_weight():
+    """With bf16_weights each q*s is rounded to bf16 once: a weight 1 + 2^-8 (a tie) becomes 1."""
+    K, N = 32, 2
+    q = np.zeros((N, K), np.int16)
+    q[1, 5] = 1
+    s = np.full((N, 1), 1 + 2.0 ** -8, np.float64).astype(np.float16)   # 1.00390625, exact in fp16
+    w = synth.qweight_from_q(q, s, synth.FMT_Q8)
+    x = synth.bf16_bits(np.eye(1, K, 5))          # x = e_5
+    idx = np.array([0], np.int32)
+    ye, _ = oracle.moe_entries(x, idx, [w.wq], [w.scales], 1, synth.FMT_Q8, [0], [1])
+    yb, _ = oracle.moe_entries(x, idx, [w.wq], [w.scales], 1, synth.FMT_Q8, [0], [1], bf16_weights=True)
+    assert ye[0] == 1 + 2.0 ** -8 and yb[0] == 1.0
+
+
+# ---------------------------------------------------------------------------
+# bar_ratio: every GPU parity assertion goes through it
+# ---------------------------------------------------------------------------
+
+def test_bar_ratio_closed_forms():
+    # the relative term alone: err 1 against 1e-3 * 1000 + 1e-6
+    assert oracle.bar_ratio([1.0], [0.0], [1000.0]) == 1.0 / (1.0 + 1e-6)
+    # the absolute term alone: zero bound, err 2e-6 -> ratio 2
+    assert math.isclose(oracle.bar_ratio([2e-6], [0.0], [0.0]), 2.0, rel_tol=1e-12)
+    # sign of the error does not matter; the largest ratio wins, not the largest error
+    r = oracle.bar_ratio([5.0, -0.5, 3.0], [4.0, 0.0, 3.0], [1e6, 100.0, 0.0])
+    assert math.isclose(r, 0.5 / (0.1 + 1e-6), rel_tol=1e-12)
+    # explicit tolerances take their roles
+    assert math.isclose(oracle.bar_ratio([3.0], [1.0], [10.0], rel=0.1, abs_=1.0), 1.0, rel_tol=1e-12)
+    assert math.isclose(oracle.bar_ratio([3.0], [1.0], [1.0], rel=1.0, abs_=0.0), 2.0, rel_tol=1e-12)
+    # non-finite results fail; an empty comparison passes
+    assert oracle.bar_ratio([1.0, np.nan], [1.0, 0.0], [1.0, 1.0]) == math.inf
+    assert oracle.bar_ratio([np.inf], [0.0], [1.0]) == math.inf
+    assert oracle.bar_ratio(np.zeros(0), np.zeros(0), np.zeros(0)) == 0.0
+    assert oracle.bar_ratio([7.0], [7.0], [0.0]) == 0.0
+
+
+def test_bar_ratio_agrees_with_within_bar():
+    rng = synth.rng_for(24)
+    for trial in range(50):
+        bound = rng.uniform(0.0, 10.0, 64) * (rng.random(64) < 0.8)
+        y_ref = rng.standard_normal(64)
+        y = y_ref + rng.choice([-1, 1], 64) * (1e-3 * bound + 1e-6) * rng.uniform(0.0, 1.0 + 0.3 * (trial % 2), 64)
+        r = oracle.bar_ratio(y, y_ref, bound)
+        assert (r <= 1.0) == bool(oracle.within_bar(y, y_ref, bound).all())

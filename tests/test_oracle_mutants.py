@@ -98,6 +98,44 @@ def _combine_wrong_slot(y2, route_w, topk, bound2=None):
 
 
 _orig_combine = qo.combine
+_orig_moe_entries = qo.moe_entries
+_orig_bar_ratio = qo.bar_ratio
+
+
+def _entries_gather_by_assignment(x_bits, idx, wq_list, s_list, topk, fmt, assigns, cols, bf16_weights=False):
+    # reads x[a] (clamped to the token count) instead of x[a // topk]
+    a = np.asarray(assigns, np.int64)
+    xb = np.asarray(x_bits)
+    rows = np.minimum(a, xb.shape[0] - 1)
+    # route through the real function with topk=1 on a row table that picks x[rows]
+    return _orig_moe_entries(xb[rows], np.asarray(idx)[a], wq_list, s_list, 1, fmt, np.arange(a.size), cols,
+                             bf16_weights)
+
+
+def _entries_expert_of_token(x_bits, idx, wq_list, s_list, topk, fmt, assigns, cols, bf16_weights=False):
+    # takes the expert of slot a // topk instead of slot a
+    idx = np.asarray(idx, np.int64)
+    wrong = idx[np.asarray(assigns, np.int64) // topk]
+    fake = idx.copy()
+    fake[np.asarray(assigns, np.int64)] = wrong
+    return _orig_moe_entries(x_bits, fake, wq_list, s_list, topk, fmt, assigns, cols, bf16_weights)
+
+
+def _bar_ratio_swapped(y, y_ref, bound, rel=qo.TOL_REL, abs_=qo.TOL_ABS):
+    return _orig_bar_ratio(y, y_ref, bound, abs_, rel)
+
+
+def _bar_ratio_no_abs(y, y_ref, bound, rel=qo.TOL_REL, abs_=qo.TOL_ABS):
+    with np.errstate(divide="ignore", invalid="ignore"):
+        return _orig_bar_ratio(y, y_ref, bound, rel, 0.0)
+
+
+def _bar_ratio_ignores_nan(y, y_ref, bound, rel=qo.TOL_REL, abs_=qo.TOL_ABS):
+    y = np.asarray(y, np.float64)
+    if y.size == 0:
+        return 0.0
+    err = np.abs(y - np.asarray(y_ref, np.float64))
+    return float(np.nanmax(np.where(np.isfinite(err), err, np.nan) / (rel * np.asarray(bound, np.float64) + abs_)))
 
 MUTANTS = {
     "q4_nibbles_swapped": ("decode_q", _q4_swapped),
@@ -111,6 +149,11 @@ MUTANTS = {
     "silu_sign": ("silu", _silu_wrong_sign),
     "moe_gather_row": ("moe", _moe_gather_by_assignment),
     "combine_slot": ("combine", _combine_wrong_slot),
+    "moe_entries_gather_row": ("moe_entries", _entries_gather_by_assignment),
+    "moe_entries_expert_of_token": ("moe_entries", _entries_expert_of_token),
+    "bar_ratio_rel_abs_swapped": ("bar_ratio", _bar_ratio_swapped),
+    "bar_ratio_no_abs_term": ("bar_ratio", _bar_ratio_no_abs),
+    "bar_ratio_ignores_nan": ("bar_ratio", _bar_ratio_ignores_nan),
 }
 
 
@@ -124,11 +167,14 @@ def _pins():
               (td.test_one_hot_pins_column_mapping, dict(fmt=fmt, n0=1, k0=95)),
               (td.test_one_hot_scale_block_pins_block_index, dict(fmt=fmt, blk=1)),
               (tm.test_moe_exact_rational_tiny, dict(fmt=fmt)),
+              (tm.test_moe_entries_exact_rational, dict(fmt=fmt)),
+              (tm.test_moe_entries_match_moe, dict(fmt=fmt, bf16_weights=False)),
               (tm.test_moe_ffn_weighted_per_expert_dense_loop, dict(fmt=fmt))]
     p += [(td.test_nibble_order_low_nibble_first, {}), (td.test_q4_decode_every_nibble, {}),
           (td.test_q8_extremes_and_fp16_max_scale, dict(qv=-128)), (td.test_bf16_decode_known_patterns, {}),
           (tm.test_silu_closed_forms, {}), (tm.test_bf16_rounding_closed_forms, {}),
-          (tm.test_combine_closed_forms, {})]
+          (tm.test_combine_closed_forms, {}), (tm.test_bar_ratio_closed_forms, {}),
+          (tm.test_bar_ratio_agrees_with_within_bar, {})]
     return p
 
 
