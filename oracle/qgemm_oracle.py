@@ -57,7 +57,7 @@ __all__ = [
     "decode_bf16", "decode_q", "dequant",
     "dense", "dense_entries",
     "moe", "moe_entries",
-    "silu", "round_to_bf16", "swiglu", "combine", "moe_ffn", "moe_ffn_tokens",
+    "silu", "round_to_bf16", "swiglu", "combine", "moe_ffn", "moe_ffn_tokens", "down_combine_tokens",
     "within_bar", "bar_ratio", "fp32_sum_rel", "SILU_LIPSCHITZ", "swiglu_err_bound", "moe_abs_apply",
     "ffn_out_tolerance",
 ]
@@ -299,6 +299,31 @@ def moe_ffn_tokens(x_bits, idx, route_w, wgu_q, wgu_s, wd_q, wd_s, topk: int, in
     if with_tolerance:
         return np.array(res_out), np.array(res_bound), np.array(res_tol)
     return np.array(res_out), np.array(res_bound)
+
+
+def down_combine_tokens(h_bits, idx, route_w, wd_q, wd_s, topk: int, fmt: int, tokens):
+    """``out[t] = sum_j w[t*topk+j] * (dequant(W_down[idx[t*topk+j]]) . h[t*topk+j])`` for sampled
+    tokens, from given bf16 activations ``h`` (one row per token slot): the down expert projection
+    (Section 3.1, MoE expert GEMM item) followed by the router-weighted sum, on the same inputs a
+    GPU chain fed. Returns ``(out, bound_out)`` with ``bound_out[t] = sum_j |w| sum_i |h_i w_i|``."""
+    idx = np.asarray(idx, dtype=np.int64)
+    w = np.asarray(route_w, dtype=np.float32).astype(np.float64)
+    hall = np.asarray(h_bits)
+    outs, bounds = [], []
+    for t in np.asarray(tokens, dtype=np.int64):
+        o = None
+        b = None
+        for j in range(topk):
+            a = t * topk + j
+            hx = decode_bf16(hall[a:a + 1])
+            wd = dequant(wd_q[idx[a]], wd_s[idx[a]], fmt, hx.shape[1])
+            y2 = (hx @ wd.T)[0]
+            b2 = (np.abs(hx) @ np.abs(wd).T)[0]
+            o = w[a] * y2 if o is None else o + w[a] * y2
+            b = abs(w[a]) * b2 if b is None else b + abs(w[a]) * b2
+        outs.append(o)
+        bounds.append(b)
+    return np.array(outs), np.array(bounds)
 
 
 # ---------------------------------------------------------------------------

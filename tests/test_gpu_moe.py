@@ -199,12 +199,12 @@ def moe_ffn_gpu(torch, case, split=False):
         y2 = m.moe(h, idx, off, wd, sd, 1, case.fmt)
     out = m.moe_combine(y2, rw, r.topk)
     torch.cuda.synchronize()
-    return y1.cpu().numpy(), out.cpu().numpy()
+    return y1.cpu().numpy(), out.cpu().numpy(), h.cpu().view(torch.int16).numpy().view(np.uint16)
 
 
 def check_moe_case(torch, case, n_tokens, n_samples, split=False):
     r = case.routing
-    y1, out = moe_ffn_gpu(torch, case, split)
+    y1, out, h = moe_ffn_gpu(torch, case, split)
     assert np.isfinite(y1).all() and np.isfinite(out).all()
     wq = [w.wq for w in case.w_gate_up]
     ws = [w.scales for w in case.w_gate_up]
@@ -221,20 +221,30 @@ def check_moe_case(torch, case, n_tokens, n_samples, split=False):
     o_ref, o_b, o_tol = oracle.moe_ffn_tokens(case.x, r.token_expert_idx, r.route_w, wq, ws,
                                               [w.wq for w in case.w_down], [w.scales for w in case.w_down],
                                               r.topk, case.inter, case.fmt, toks, with_tolerance=True)
-    check_chain(case.name + " ffn out (sampled tokens)", out[toks], o_ref, o_b, o_tol)
+    s_ref, s_b = oracle.down_combine_tokens(h, r.token_expert_idx, r.route_w, [w.wq for w in case.w_down],
+                                            [w.scales for w in case.w_down], r.topk, case.fmt, toks)
+    check_chain(case.name + " ffn out (sampled tokens)", out[toks], o_ref, o_b, o_tol, s_ref, s_b)
 
 
-def check_chain(name, out, o_ref, o_b, o_tol):
-    """FFN output against the oracle's own chain: the plain acceptance bar with the router-weighted
-    bound (|out - out_ref| <= 1e-3 * sum_j |w_j| sum_i |h_i W_down| + 1e-6), and, tighter in the
-    direction that matters for a wrong h, the tolerance that carries each GEMM's bar through SiLU
-    and the bf16 rounding of h."""
-    r_tol = float(np.max(np.abs(out - o_ref) / o_tol)) if np.isfinite(out).all() else float("inf")
-    r_bar = oracle.bar_ratio(out, o_ref, o_b)
-    print(f"[parity] {name}: plain 1e-3 bar ratio = {r_bar:.3e}; ratio to propagated tolerance = {r_tol:.3e}",
-          flush=True)
+def check_chain(name, out, o_ref, o_b, o_tol, s_ref, s_b):
+    """The MoE FFN output ``out`` (router-weighted sum of the down projections):
+
+    * the plain acceptance bar ``|out - ref| <= 1e-3 * sum_j |w_j| sum_i |h_i W_down| + 1e-6``
+      against the oracle's down projection + combine fed the same bf16 activations ``h`` as the
+      GPU (s_ref, s_b): the bar on the same inputs, as for every GEMM;
+    * against the oracle's own chain from x (o_ref), the tolerance that carries each GEMM's bar
+      through SiLU and the bf16 rounding of h (o_tol). The plain bar against that chain is
+      reported, not required: both sides round h to bf16, and where the GPU's gate/up output
+      (within its own bar) sits across a rounding boundary from the exact one, the two h differ
+      by a whole bf16 unit; carried through W_down that can exceed 1e-3 of the bound."""
     assert np.isfinite(out).all()
-    assert r_bar <= 1.0, f"{name}: FFN output exceeds the acceptance bar ({r_bar})"
+    r_same = oracle.bar_ratio(out, s_ref, s_b)
+    r_tol = float(np.max(np.abs(out - o_ref) / o_tol))
+    r_end = oracle.bar_ratio(out, o_ref, o_b)
+    print(f"[parity] {name}: plain 1e-3 bar ratio on the same h = {r_same:.3e}; "
+          f"ratio to propagated tolerance from x = {r_tol:.3e} (plain bar against the oracle's own h, "
+          f"not required: {r_end:.3e})", flush=True)
+    assert r_same <= 1.0, f"{name}: FFN output exceeds the acceptance bar on the same h ({r_same})"
     assert r_tol <= 1.0, f"{name}: FFN output exceeds the propagated tolerance ({r_tol})"
 
 
@@ -282,7 +292,7 @@ def test_moe_ffn_full_oracle_medium():
     """Whole FFN chain on a medium shape, every output element against the oracle."""
     torch = torch_or_skip()
     case = synth.moe_case("moe_medium", synth.FMT_Q4, 160, 16, 4, 1024, 768, skew=0.8, seed=2, stream=(77,))
-    y1, out = moe_ffn_gpu(torch, case)
+    y1, out, h = moe_ffn_gpu(torch, case)
     r = case.routing
     Q = lambda L: [w.wq for w in L]  # noqa: E731
     S = lambda L: [w.scales for w in L]  # noqa: E731
@@ -293,7 +303,9 @@ def test_moe_ffn_full_oracle_medium():
     check_levels("moe_medium y1", y1, (res["y1"], res["bound1"]), y1b, case.hidden, True)
     tol = oracle.ffn_out_tolerance(res, r.token_expert_idx, r.route_w, Q(case.w_down), S(case.w_down), r.topk,
                                    case.inter, case.fmt)
-    check_chain("moe_medium out", out, res["out"], res["bound_out"], tol)
+    y2h, b2h = oracle.moe(h, r.token_expert_idx, r.expert_offsets, Q(case.w_down), S(case.w_down), 1, case.fmt)
+    s_ref, s_b = oracle.combine(y2h, r.route_w, r.topk, b2h)
+    check_chain("moe_medium out", out, res["out"], res["bound_out"], tol, s_ref, s_b)
     # the down projection alone, on the oracle's own activations h (same inputs on both sides)
     wd, sd = dev_experts(torch, case.w_down)
     y2 = q().moe(dev_x(torch, res["h_bits"]), dev_i32(torch, r.token_expert_idx), dev_i32(torch, r.expert_offsets),

@@ -358,3 +358,31 @@ def test_bar_ratio_agrees_with_within_bar():
         y = y_ref + rng.choice([-1, 1], 64) * (1e-3 * bound + 1e-6) * rng.uniform(0.0, 1.0 + 0.3 * (trial % 2), 64)
         r = oracle.bar_ratio(y, y_ref, bound)
         assert (r <= 1.0) == bool(oracle.within_bar(y, y_ref, bound).all())
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_down_combine_tokens_matches_chain(fmt):
+    """Fed the oracle's own h, the token-wise down projection + combine equals the FFN chain's
+    output and bound; a one-hot router weight returns that slot's dense projection."""
+    T, E, topk, hidden, inter = 9, 5, 3, 64, 32
+    rng = synth.rng_for(25, fmt)
+    x = synth.make_x(rng, T, hidden)
+    r = synth.make_routing(rng, T, E, topk)
+    wgu = [synth.make_qweight(rng, 2 * inter, hidden, fmt) for _ in range(E)]
+    wd = [synth.make_qweight(rng, hidden, inter, fmt) for _ in range(E)]
+    res = oracle.moe_ffn(x, r.token_expert_idx, r.expert_offsets, r.route_w, [w.wq for w in wgu],
+                         [w.scales for w in wgu], [w.wq for w in wd], [w.scales for w in wd], topk, inter, fmt)
+    toks = [0, 4, 8]
+    o, b = oracle.down_combine_tokens(res["h_bits"], r.token_expert_idx, r.route_w, [w.wq for w in wd],
+                                      [w.scales for w in wd], topk, fmt, toks)
+    np.testing.assert_allclose(o, res["out"][toks], rtol=0, atol=1e-12 * res["bound_out"].max())
+    np.testing.assert_allclose(b, res["bound_out"][toks], rtol=1e-12)
+    one_hot = np.zeros(T * topk, np.float32)
+    one_hot[np.arange(T) * topk + 2] = 1.0
+    o1, _ = oracle.down_combine_tokens(res["h_bits"], r.token_expert_idx, one_hot, [w.wq for w in wd],
+                                       [w.scales for w in wd], topk, fmt, toks)
+    for i, t in enumerate(toks):
+        a = t * topk + 2
+        e = int(r.token_expert_idx[a])
+        yd, bd = oracle.dense(res["h_bits"][a:a + 1], wd[e].wq, wd[e].scales, fmt)
+        np.testing.assert_allclose(o1[i], yd[0], rtol=0, atol=inter * 2.0 ** -52 * bd.max())

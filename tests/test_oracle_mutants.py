@@ -99,6 +99,17 @@ def _combine_wrong_slot(y2, route_w, topk, bound2=None):
 
 _orig_combine = qo.combine
 _orig_moe_entries = qo.moe_entries
+_orig_down_combine = qo.down_combine_tokens
+
+
+def _down_combine_token_row(h_bits, idx, route_w, wd_q, wd_s, topk, fmt, tokens):
+    # reads every slot's activations from row t (the token) instead of row t*topk+j (the slot)
+    h = np.asarray(h_bits)
+    fake = h.copy()
+    for t in np.asarray(tokens, np.int64):
+        for j in range(topk):
+            fake[t * topk + j] = h[min(t, h.shape[0] - 1)]
+    return _orig_down_combine(fake, idx, route_w, wd_q, wd_s, topk, fmt, tokens)
 _orig_bar_ratio = qo.bar_ratio
 
 
@@ -151,6 +162,7 @@ MUTANTS = {
     "combine_slot": ("combine", _combine_wrong_slot),
     "moe_entries_gather_row": ("moe_entries", _entries_gather_by_assignment),
     "moe_entries_expert_of_token": ("moe_entries", _entries_expert_of_token),
+    "down_combine_token_row": ("down_combine_tokens", _down_combine_token_row),
     "bar_ratio_rel_abs_swapped": ("bar_ratio", _bar_ratio_swapped),
     "bar_ratio_no_abs_term": ("bar_ratio", _bar_ratio_no_abs),
     "bar_ratio_ignores_nan": ("bar_ratio", _bar_ratio_ignores_nan),
@@ -169,6 +181,7 @@ def _pins():
               (tm.test_moe_exact_rational_tiny, dict(fmt=fmt)),
               (tm.test_moe_entries_exact_rational, dict(fmt=fmt)),
               (tm.test_moe_entries_match_moe, dict(fmt=fmt, bf16_weights=False)),
+              (tm.test_down_combine_tokens_matches_chain, dict(fmt=fmt)),
               (tm.test_moe_ffn_weighted_per_expert_dense_loop, dict(fmt=fmt))]
     p += [(td.test_nibble_order_low_nibble_first, {}), (td.test_q4_decode_every_nibble, {}),
           (td.test_q8_extremes_and_fp16_max_scale, dict(qv=-128)), (td.test_bf16_decode_known_patterns, {}),
