@@ -73,6 +73,9 @@ def parse():
                     help="time the step without per-launch events (then no roofline figure)")
     ap.add_argument("--unfused", action="store_true",
                     help="MoE gate/up to fp32 then a separate SwiGLU kernel instead of the fused epilogue")
+    ap.add_argument("--combine", choices=("fused", "separate"), default="separate",
+                    help="router-weighted combine fused into the down projection (qgemm_moe_down_combine) or "
+                         "a separate pass over the per-slot rows (qgemm_moe_grouped + qgemm_moe_combine)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (for scaling HBM byte counters) and exit")
     ap.add_argument("--only", default="", help="comma list of parts to run: dense_gate_up,dense_down,moe_t2048,moe_t8192")
@@ -98,7 +101,7 @@ class Part:
         self.flops = flops
 
 
-def build_parts(torch, q, synth, only, fused=True):
+def build_parts(torch, q, synth, only, fused=True, fused_combine=True):
     """Device-resident inputs and output buffers for every part of the step."""
     dev = torch.device("cuda:0")
 
@@ -143,6 +146,7 @@ def build_parts(torch, q, synth, only, fused=True):
         p.td = q.ExpertTable(p.wd, p.sd, case.fmt)
         p.perm = torch.empty((A,), dtype=torch.int32, device=dev)
         p.fused = fused
+        p.fused_combine = fused_combine
         p.y1 = None if fused else torch.empty((A, 2 * case.inter), dtype=torch.float32, device=dev)
         p.h = torch.empty((A, case.inter), dtype=torch.bfloat16, device=dev)
         p.y2 = torch.empty((A, case.hidden), dtype=torch.float32, device=dev)
@@ -168,9 +172,13 @@ def run_part(q, p, timer=None):
         with timer(p.name + ":gate_up"):
             q.moe_grouped(p.x, p.perm, p.off, p.tgu, None, c.topk, c.fmt, out=p.y1)
         q.swiglu(p.y1, out=p.h)
-    with timer(p.name + ":down"):
-        q.moe_grouped(p.h, p.perm, p.off, p.td, None, 1, c.fmt, out=p.y2)
-    q.moe_combine(p.y2, p.rw, c.topk, out=p.out)
+    if p.fused_combine:
+        with timer(p.name + ":down"):
+            q.moe_down_combine(p.h, p.perm, p.off, p.td, None, p.rw, c.topk, c.fmt, y2=p.y2, out=p.out)
+    else:
+        with timer(p.name + ":down"):
+            q.moe_grouped(p.h, p.perm, p.off, p.td, None, 1, c.fmt, out=p.y2)
+        q.moe_combine(p.y2, p.rw, c.topk, out=p.out)
 
 
 class EventTimer:
@@ -359,7 +367,7 @@ def prewarm(torch, q, parts, min_s, tol, max_s):
 MOE_T128_COPIES = 4        # expert weight sets cycled: 4 x ~135 MB of active experts > the 256 MiB last-level cache
 
 
-def moe_t128_section(torch, q, synth, launches):
+def moe_t128_section(torch, q, synth, launches, fused_combine=True):
     """Per-launch time of the T=128 skewed MoE projections, weights read from HBM (sets rotated)."""
     dev = torch.device("cuda:0")
     ev = lambda: torch.cuda.Event(enable_timing=True)
@@ -386,11 +394,17 @@ def moe_t128_section(torch, q, synth, launches):
                                              out=h)
     down = lambda i: q.moe_grouped(h, perm, off, sets[i % MOE_T128_COPIES][1], None, 1, case.fmt, out=y2)
 
+    down_cmb = lambda i: q.moe_down_combine(h, perm, off, sets[i % MOE_T128_COPIES][1], None, rw, case.topk, case.fmt,
+                                            y2=y2, out=out)
+
     def ffn(i):
         q.moe_bucket(idx, off, out=perm)
         gate_up(i)
-        down(i)
-        q.moe_combine(y2, rw, case.topk, out=out)
+        if fused_combine:
+            down_cmb(i)
+        else:
+            down(i)
+            q.moe_combine(y2, rw, case.topk, out=out)
 
     def per_launch(fn):
         for i in range(2 * MOE_T128_COPIES):
@@ -404,7 +418,7 @@ def moe_t128_section(torch, q, synth, launches):
         torch.cuda.synchronize()
         return first.elapsed_time(last) / launches * 1e3
 
-    us_gu, us_dn, us_ffn = per_launch(gate_up), per_launch(down), per_launch(ffn)
+    us_gu, us_dn, us_dc, us_ffn = per_launch(gate_up), per_launch(down), per_launch(down_cmb), per_launch(ffn)
     packed = lambda n, k: n * k // 2 + n * (k // 32) * 2       # Q4 bytes + fp16 scales of one expert
     b_gu = active * packed(2 * case.inter, case.hidden) + 2 * case.T * case.hidden + 2 * A * case.inter
     b_dn = active * packed(case.hidden, case.inter) + 2 * A * case.inter + 4 * A * case.hidden
@@ -415,6 +429,7 @@ def moe_t128_section(torch, q, synth, launches):
                      "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_hbm": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS,
                      "TFLOP/s": flops / (us * 1e-6) / 1e12})
         log(f"MoE T=128 {name}: {us:.1f} us/launch, {rows[-1]['GB/s']:.0f} GB/s")
+    log(f"MoE T=128 down + fused combine: {us_dc:.1f} us/launch")
     log(f"MoE T=128 FFN (bucketing, both projections, combine): {us_ffn:.1f} us")
     del sets
     torch.cuda.empty_cache()
@@ -422,7 +437,8 @@ def moe_t128_section(torch, q, synth, launches):
             "active_experts": active, "rows_per_active_expert": [int(counts[counts > 0].min()),
                                                                  int(counts[counts > 0].max())],
             "bound": "hbm", "peak": PEAK_HBM_GBS, "unit": "GB/s", "weight_sets_rotated": MOE_T128_COPIES,
-            "projections": rows, "ffn_us_per_launch": us_ffn, "launches": launches}
+            "projections": rows, "down_fused_combine_us_per_launch": us_dc, "ffn_us_per_launch": us_ffn,
+            "combine": "fused into the down projection" if fused_combine else "separate kernel", "launches": launches}
 
 
 def attention_section(torch, q, synth, launches):
@@ -565,14 +581,15 @@ def main():
         print(json.dumps({"small_m": small_m_section(torch, q, synth, args.small_m_launches)}), flush=True)
         return 0
     if args.moe_t128_only:
-        print(json.dumps({"moe_t128": moe_t128_section(torch, q, synth, args.moe_t128_launches)}), flush=True)
+        print(json.dumps({"moe_t128": moe_t128_section(torch, q, synth, args.moe_t128_launches,
+                                                                args.combine == "fused")}), flush=True)
         return 0
     if args.dense_configs_only:
         print(json.dumps(dense_configs_section(torch, q, synth, args.dense_config_launches)), flush=True)
         return 0
     log("generating inputs")
     t0 = time.perf_counter()
-    parts = build_parts(torch, q, synth, args.only, fused=not args.unfused)
+    parts = build_parts(torch, q, synth, args.only, fused=not args.unfused, fused_combine=args.combine == "fused")
     torch.cuda.synchronize()
     log(f"inputs resident in HBM ({time.perf_counter() - t0:.1f} s)")
     pre = prewarm(torch, q, parts, args.prewarm_min_s, args.prewarm_tol, args.prewarm_max_s)
@@ -649,7 +666,7 @@ def main():
     t128 = None
     if args.moe_t128_launches > 0 and not args.only:
         log("MoE FFN at T=128 (HBM-bound tail)")
-        t128 = moe_t128_section(torch, q, synth, args.moe_t128_launches)
+        t128 = moe_t128_section(torch, q, synth, args.moe_t128_launches, args.combine == "fused")
 
     attn = None
     if args.attention_launches > 0 and not args.only:
@@ -669,6 +686,7 @@ def main():
                                "MoE Q4 FFN T=2048 E=128 top8 + MoE Q4 FFN T=8192 E=128 top8 Zipf-skewed"
                                if not args.only else args.only,
                    "moe_swiglu": "separate kernel" if args.unfused else "fused into gate/up epilogue",
+                   "moe_combine": "fused into the down projection" if args.combine == "fused" else "separate kernel",
                    "frac_of_mfma_peak": value / PEAK_BF16_TFLOPS, "flop_per_step": flops_step},
         "roofline": roofline,
         "cpu_baseline": cpu,

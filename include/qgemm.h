@@ -150,6 +150,34 @@ int qgemm_moe_gate_up_swiglu(const void* x, const int32_t* perm, const int32_t* 
                              hipStream_t stream);
 
 /*
+ * MoE down projection with the router-weighted combine fused into it (the
+ * MoE expert GEMM of Section 3.1 over the SiLU-gated activations, followed by
+ * the weighted sum of each token's selected experts):
+ *   y2[a][:] = dequant(wq[e], scales[e]) . h[a][:]        (a routed to expert e)
+ *   out[t][n] = sum_{j < topk} route_w[t*topk + j] * y2[t*topk + j][n]
+ * h: bf16 [T*topk][K], one row per token slot (as qgemm_moe_gate_up_swiglu
+ * writes it); perm, expert_offsets: as for qgemm_moe_grouped over the T*topk
+ * slots; wq, scales: HOST arrays of E device pointers, each [N][K] as for
+ * qgemm_dense; route_w: fp32 [T*topk]; y2: fp32 [T*topk][N], caller-owned,
+ * written with exactly the values qgemm_moe_grouped(h, perm, ..., topk = 1)
+ * writes; out: fp32 [T][N], bitwise equal to qgemm_moe_combine(y2, route_w)
+ * (each sum runs in increasing j from zero with fp32 fused multiply-adds).
+ * The tile that stores the last of a token's topk slot rows for a column tile
+ * sums them there, so the separate combine pass over y2 disappears; results
+ * do not depend on which tile that is. Arrival counters live in a
+ * library-owned workspace (grown on first use, freed by qgemm_release) and
+ * are cleared by a kernel at the start of every call; calls that share it are
+ * ordered only by their streams.
+ * Sizes: as for qgemm_moe_grouped with T*topk rows; N % 4 == 0; y2 spans less
+ * than 4 GiB (T*topk*N*4 bytes, else QGEMM_EUNSUPPORTED). Tokens whose slots
+ * are not all present in perm (inconsistent routing tables) are not written.
+ */
+int qgemm_moe_down_combine(const void* h, const int32_t* perm, const int32_t* expert_offsets,
+                           const void* const* wq, const void* const* scales, const float* route_w,
+                           float* y2, float* out, int T, int E, int topk, int N, int K, int fmt,
+                           hipStream_t stream);
+
+/*
  * SiLU-gated activation between the MoE projections (Section 3.1, fused
  * gate/up item): for r < rows, i < inter,
  *   h[r][i] = bf16_rne(silu(y1[r][i]) * y1[r][inter + i]),  silu(z) = z / (1 + e^-z)

@@ -16,7 +16,7 @@ import os
 import torch  # imported before the library so that both share one HIP runtime
 
 __all__ = ["Q8", "Q4", "QGemmError", "lib", "lib_path", "dense", "moe", "moe_bucket", "moe_grouped",
-           "moe_gate_up_swiglu", "swiglu", "moe_combine", "attention_prefill", "probe_mfma_clock", "last_error", "release", "version", "EXPORTS", "ExpertTable"]
+           "moe_gate_up_swiglu", "moe_down_combine", "swiglu", "moe_combine", "attention_prefill", "probe_mfma_clock", "last_error", "release", "version", "EXPORTS", "ExpertTable"]
 
 Q8 = 0
 Q4 = 1
@@ -32,6 +32,7 @@ EXPORTS = {
     "qgemm_moe_bucket": (_i, [_vp, _vp, _vp, _i, _i, _vp]),
     "qgemm_moe_grouped": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "qgemm_moe_gate_up_swiglu": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "qgemm_moe_down_combine": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "qgemm_swiglu": (_i, [_vp, _vp, _i, _i, _vp]),
     "qgemm_moe_combine": (_i, [_vp, _vp, _vp, _i, _i, _i, _vp]),
     "qgemm_attention_prefill": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, ctypes.c_float, _i, _vp]),
@@ -256,6 +257,37 @@ def moe_gate_up_swiglu(x, perm, expert_offsets, wq, scales, topk: int, fmt: int,
     _check(lib().qgemm_moe_gate_up_swiglu(x.data_ptr(), perm.data_ptr(), expert_offsets.data_ptr(), wp, sp,
                                           out.data_ptr(), T, E, topk, inter, K, fmt, _stream(x)))
     return out
+
+
+def moe_down_combine(h, perm, expert_offsets, wq, scales, route_w, topk: int, fmt: int, y2=None, out=None):
+    """Down projection over token slots with the router-weighted combine fused in
+    (``qgemm_moe_down_combine``): returns ``(y2 [T*topk][N], out [T][N])``, both fp32.
+    ``wq`` may be an ExpertTable."""
+    _need(h, "h", (torch.bfloat16,), 2)
+    _need(perm, "perm", (torch.int32,), 1)
+    _need(expert_offsets, "expert_offsets", (torch.int32,), 1)
+    _need(route_w, "route_w", (torch.float32,), 1)
+    A, K = h.shape
+    if A % topk != 0 or route_w.shape[0] != A:
+        raise ValueError("h and route_w need T*topk rows")
+    T = A // topk
+    E = expert_offsets.shape[0] - 1
+    wq, scales, wp, sp = _expert_tables(wq, scales, E)
+    N = wq[0].shape[0]
+    if any(_wshape_k(w, fmt) != K or w.shape[0] != N for w in wq):
+        raise ValueError("expert weights disagree with h on K or with each other on N")
+    if y2 is None:
+        y2 = torch.empty((A, N), dtype=torch.float32, device=h.device)
+    if out is None:
+        out = torch.empty((T, N), dtype=torch.float32, device=h.device)
+    _need(y2, "y2", (torch.float32,), 2)
+    _need(out, "out", (torch.float32,), 2)
+    if y2.shape != (A, N) or out.shape != (T, N):
+        raise ValueError("y2 must be [T*topk][N] and out [T][N]")
+    _check(lib().qgemm_moe_down_combine(h.data_ptr(), perm.data_ptr(), expert_offsets.data_ptr(), wp, sp,
+                                        route_w.data_ptr(), y2.data_ptr(), out.data_ptr(), T, E, topk, N, K, fmt,
+                                        _stream(h)))
+    return y2, out
 
 
 def swiglu(y1, out=None):

@@ -181,7 +181,7 @@ int dense_dispatch(qg::TileArgs a, const void* wq, const void* sc, hipStream_t s
   return launch_dense<FMT, 128, 128, 2, 2, 2>(a, wq, sc, s);
 }
 
-template <int FMT, int BM, int BN, int WM, int WN, int XS, bool SWI>
+template <int FMT, int BM, int BN, int WM, int WN, int XS, bool SWI, bool CMB>
 int launch_moe_cfg(qg::TileArgs a, const void* const* wq, const void* const* sc, int E, hipStream_t s) {
   const int nt = SWI ? (a.swi_inter + BN / 2 - 1) / (BN / 2) : (a.N + BN - 1) / BN;
   for (int e0 = 0; e0 < E; e0 += qg::kMaxExpertsPerLaunch) {
@@ -194,12 +194,13 @@ int launch_moe_cfg(qg::TileArgs a, const void* const* wq, const void* const* sc,
     a.e_begin = e0;
     a.n_experts = ne;
     // upper bound of sum_e ceil(c_e / BM) over the launch's experts (m-tile groups), rounded up
-    // to the 8 XCDs; workgroups past the real group count exit at once
+    // to whole runs on all 8 XCDs; workgroups past the real group count exit at once
     const long mt_bound = (long)(a.M + BM - 1) / BM + ne;
-    const long grid = (mt_bound + 7) / 8 * 8 * nt;
+    constexpr long kDeal = 8L * qg::kMoeRun;   // groups per round over the 8 XCDs
+    const long grid = (mt_bound + kDeal - 1) / kDeal * kDeal * nt;
     if (grid > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "too many tiles");
-    hipLaunchKernelGGL((qg::moe_kernel<FMT, BM, BN, WM, WN, XS, SWI>), dim3((unsigned)grid), dim3(WM * WN * 64), 0, s,
-                       a, ep);
+    hipLaunchKernelGGL((qg::moe_kernel<FMT, BM, BN, WM, WN, XS, SWI, CMB>), dim3((unsigned)grid), dim3(WM * WN * 64), 0,
+                       s, a, ep);
     const int rc = check_launch("qgemm_moe");
     if (rc != QGEMM_OK) return rc;
   }
@@ -212,12 +213,16 @@ int launch_moe_cfg(qg::TileArgs a, const void* const* wq, const void* const* sc,
 // twice the workgroups of the 256-wide tiles over the few active experts' weights, so the
 // CUs fill (measured at T=128, E=128, top-8: gate/up + SiLU 66.5 against 73 us, down 31
 // against 34 us; at T=2048 the same tile is slower, 196 against 159 us and 125 against 108 us).
-template <int FMT, bool SWI = false>
+// Column tile width of the configuration launch_moe picks (the fused combine counts arrivals per
+// (token, column tile)).
+inline int moe_tile_bn(long M, int E) { return (M / E) <= 32 ? 128 : 256; }
+
+template <int FMT, bool SWI = false, bool CMB = false>
 int launch_moe(qg::TileArgs a, const void* const* wq, const void* const* sc, int E, hipStream_t s) {
   const long mean_rows = (long)a.M / E;
-  if (mean_rows <= 32) return launch_moe_cfg<FMT, 128, 128, 2, 2, 2, SWI>(a, wq, sc, E, s);
-  if (mean_rows > 192) return launch_moe_cfg<FMT, 256, 256, 2, 4, 2, SWI>(a, wq, sc, E, s);
-  return launch_moe_cfg<FMT, 192, 256, 2, 4, 2, SWI>(a, wq, sc, E, s);
+  if (mean_rows <= 32) return launch_moe_cfg<FMT, 128, 128, 2, 2, 2, SWI, CMB>(a, wq, sc, E, s);
+  if (mean_rows > 192) return launch_moe_cfg<FMT, 256, 256, 2, 4, 2, SWI, CMB>(a, wq, sc, E, s);
+  return launch_moe_cfg<FMT, 192, 256, 2, 4, 2, SWI, CMB>(a, wq, sc, E, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -231,6 +236,8 @@ struct Workspace {
   size_t counts_cap = 0;
   int32_t* flag = nullptr;
   int seq = 0;
+  int32_t* arrivals = nullptr;   // fused combine: per (token, column tile) arrival counters
+  size_t arrivals_cap = 0;
 };
 
 std::mutex g_ws_mutex;
@@ -485,6 +492,57 @@ int qgemm_moe(const void* x, const int32_t* token_expert_idx, const int32_t* exp
   return ok();
 }
 
+int qgemm_moe_down_combine(const void* h, const int32_t* perm, const int32_t* expert_offsets, const void* const* wq,
+                           const void* const* scales, const float* route_w, float* y2, float* out, int T, int E,
+                           int topk, int N, int K, int fmt, hipStream_t stream) {
+  if (T < 0 || topk < 1) return fail(QGEMM_EINVAL, "T must be >= 0 and topk >= 1");
+  if ((long)T * topk > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "T*topk too large");
+  const int A = T * topk;
+  // the down projection proper: A rows of h, identity gather
+  int rc = moe_args_check(h, perm, expert_offsets, wq, scales, y2, A, E, 1, N, K, fmt);
+  if (rc != QGEMM_OK) return rc;
+  if (topk > E) return fail(QGEMM_EINVAL, "topk must lie in [1, E] (got %d)", topk);
+  if (N % 4 != 0) return fail(QGEMM_EINVAL, "N must be a multiple of 4 (got %d)", N);
+  if ((double)A * N * 4.0 >= 4294967296.0) return fail(QGEMM_EUNSUPPORTED, "y2 must span less than 4 GiB");
+  if (T == 0) return ok();
+  if (!route_w || !out) return fail(QGEMM_EINVAL, "null pointer argument");
+  if (!aligned16(route_w) || !aligned16(out)) return fail(QGEMM_EALIGN, "route_w and out must be 16-byte aligned");
+  const int bn = moe_tile_bn(A, E);
+  const long nctr = (long)T * ((N + bn - 1) / bn);
+  int32_t* ctr = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    int dev;
+    Workspace* ws = workspace_for_current_device(&dev);
+    if (!ws) return fail(QGEMM_EHIP, "hipGetDevice failed");
+    rc = grow(&ws->arrivals, &ws->arrivals_cap, (size_t)nctr);
+    if (rc != QGEMM_OK) return rc;
+    ctr = ws->arrivals;
+  }
+  (void)hipGetLastError();
+  // counters start at zero every call (a fill kernel, not a memset node, so the call can be captured)
+  hipLaunchKernelGGL(qg::fill_i32_kernel, dim3((unsigned)((nctr + 1023) / 1024)), dim3(256), 0, stream, ctr, nctr, 0);
+  rc = check_launch("qgemm_moe_down_combine (arrival counters)");
+  if (rc != QGEMM_OK) return rc;
+  qg::TileArgs a{};
+  a.x = static_cast<const uint16_t*>(h);
+  a.y = y2;
+  a.M = A;
+  a.N = N;
+  a.K = K;
+  a.perm = perm;
+  a.offsets = expert_offsets;
+  a.topk = 1;
+  a.T = A;
+  a.cmb_topk = topk;
+  a.route_w = route_w;
+  a.out = out;
+  a.counters = ctr;
+  rc = (fmt == QGEMM_Q8) ? launch_moe<qg::kQ8, false, true>(a, wq, scales, E, stream)
+                         : launch_moe<qg::kQ4, false, true>(a, wq, scales, E, stream);
+  return rc == QGEMM_OK ? ok() : rc;
+}
+
 int qgemm_swiglu(const float* y1, void* h, int rows, int inter, hipStream_t stream) {
   if (rows < 0 || inter < 8 || inter % 8 != 0)
     return fail(QGEMM_EINVAL, "rows must be >= 0 and inter a positive multiple of 8");
@@ -627,11 +685,12 @@ int qgemm_release(void) {
   (void)hipGetDevice(&cur);
   for (size_t d = 0; d < g_ws.size(); ++d) {
     Workspace& w = g_ws[d];
-    if (!w.perm && !w.counts && !w.flag) continue;
+    if (!w.perm && !w.counts && !w.flag && !w.arrivals) continue;
     (void)hipSetDevice((int)d);
     if (w.perm) (void)hipFree(w.perm);
     if (w.counts) (void)hipFree(w.counts);
     if (w.flag) (void)hipFree(w.flag);
+    if (w.arrivals) (void)hipFree(w.arrivals);
     w = Workspace{};
   }
   {

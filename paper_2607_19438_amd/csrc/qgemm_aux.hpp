@@ -194,6 +194,14 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   for (int g = 0; g < G; ++g) __builtin_nontemporal_store(acc[g], reinterpret_cast<f32x4*>(out + t * N + ncol[g]));
 }
 
+// p[i] = v for i < n, four entries per thread (clears counters without a memset node).
+__global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* __restrict__ p, long n, int v) {
+  const long i0 = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    if (i0 + k < n) p[i0 + k] = v;
+}
+
 // y[i] = sum_{s < splits} ws[s][i], summed in increasing s (deterministic); 4 floats per thread.
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ ws, float* __restrict__ y,
                                                             long n4, int splits, long stride) {

@@ -29,6 +29,11 @@ constexpr int kQ4 = 1;
 constexpr int kBK = 64;              // K elements per pipeline step (two 32-element scale blocks)
 constexpr int kRowBytes = kBK * 2;   // one bf16 tile row in LDS: 128 bytes = 8 chunks of 16 bytes
 constexpr int kMaxExpertsPerLaunch = 128;
+// Consecutive MoE m-tile groups dealt to one XCD. Runs of 2 and 4 (an expert's neighbouring groups
+// sharing an L2) measured the same launch times as 1 on the skewed T=8192 workload (gate/up 474-478
+// us, down 326-333 us) and cut its gate/up fetch only from 748 to 714 / 699 MB: the groups'
+// gathered activation rows, not the shared weights, fill the 4 MB L2.
+constexpr int kMoeRun = 1;
 
 // ---------------------------------------------------------------------------
 // small helpers
@@ -107,10 +112,6 @@ __device__ __forceinline__ void wait_vmcnt_lgkm0() {
 // s_waitcnt lgkmcnt(0) only (vector memory loads stay in flight)
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
 
-#ifndef QG_XPREFETCH
-#define QG_XPREFETCH 1
-#endif
-
 #ifndef QG_PINGPONG
 #define QG_PINGPONG 1
 #endif
@@ -150,7 +151,20 @@ struct TileArgs {
   // fused SwiGLU epilogue (MoE gate/up): N = 2 * swi_inter weight rows, h is bf16 [rows][swi_inter]
   int swi_inter;
   uint16_t* h;
+  // router-weighted combine fused into the down projection (MoE, y holds the per-slot rows):
+  // out[t][n] = sum_j route_w[t*cmb_topk+j] * y[t*cmb_topk+j][n]; arrivals counted per
+  // (token, column tile) in counters[T][ceil(N / BN)] (zero at launch)
+  int cmb_topk;
+  const float* route_w;
+  float* out;
+  int* counters;
 };
+
+// Cache policy of the fused combine's per-slot rows: device scope (sc1), so the stores write
+// through this XCD's L2 to the device-coherent level and the loads of the tile that finishes a
+// token read what tiles on other XCDs wrote.
+constexpr int kDeviceScope = 16;
+constexpr int kCmbMaxTopk = 8;   // slots whose loads one thread keeps in flight at once
 
 // Map a linear workgroup id to a tile id so that each XCD (workgroups are
 // dispatched round-robin over the 8 XCDs) works on a contiguous tile range
@@ -194,7 +208,7 @@ typedef __attribute__((address_space(3))) char lds_char;
 // the compiler can tell they do not alias and keeps the DMA in flight across them instead of
 // draining it (vmcnt) before every LDS access.
 struct LdsStages {
-  char* x[3];   // activation stages; with two stages x[2] is a 256-byte sink (the activation prefetch)
+  char* x[3];   // activation stages (x[2] unused with two stages)
   char* w[2];
 };
 
@@ -214,6 +228,84 @@ constexpr int kSchedDSWrite = 0x200;
 #define QG_K_AFTER 1
 #endif
 
+// Router-weighted combine fused into the down projection, after a tile has stored its per-slot
+// rows (columns [n0, n0 + BN)): each row counts its arrival on (token, column tile); the tile
+// whose arrival completes a token's topk slots sums that token's slot rows for these columns in
+// increasing slot order (fp32 fused multiply-add from zero, as the standalone combine does, so
+// the result is bitwise the same whichever tile finishes it) and writes out[t][n0 .. n0 + BN).
+// Every counter reaches topk once per launch sequence; nothing waits for another workgroup.
+template <int kThreads, int BM, int BN>
+__device__ __forceinline__ void combine_arrivals(const TileArgs& a, __amdgpu_buffer_rsrc_t yr,
+                                                 const int* __restrict__ s_yrow, int rows_valid, int n0,
+                                                 LdsStages st) {
+  typedef __attribute__((address_space(3))) int lds_int;
+  const int tid = threadIdx.x;
+  const int topk = a.cmb_topk;
+  const int N = a.N;
+  const int nt_n = (N + BN - 1) / BN;
+  const int nt = n0 / BN;
+  lds_int* fin = (lds_int*)st.x[0];            // tokens this tile finishes (the K loop is over)
+  lds_int* nfin = (lds_int*)st.x[1];
+  // this thread's row stores have reached the device-coherent level (and its LDS scratch reads
+  // are done); after the barrier every thread's have
+  wait_vmcnt_lgkm0<0>();
+  __syncthreads();
+  if (tid == 0) nfin[0] = 0;
+  __syncthreads();
+  static_assert(BM <= kThreads, "one thread per tile row");
+  if (tid < rows_valid) {
+    const int slot = s_yrow[tid];
+    if (slot >= 0) {
+      const int t = slot / topk;
+      const int old = __hip_atomic_fetch_add(a.counters + (size_t)t * nt_n + nt, 1, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT);
+      if (old == topk - 1) fin[__hip_atomic_fetch_add(nfin, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)] = t;
+    }
+  }
+  __syncthreads();
+  const int nf = nfin[0];
+  const int nc4 = min(BN, N - n0) >> 2;          // 16-byte column chunks of this tile (N % 4 == 0)
+  const int items = nf * nc4;
+  constexpr int U = 2;                            // (token, chunk) items per thread in flight
+  for (int base = 0; base < items; base += U * kThreads) {
+    f32x4 acc[U];
+    int t_of[U], c_of[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int it = base + u * kThreads + tid;
+      t_of[u] = it < items ? fin[it / nc4] : -1;
+      c_of[u] = it < items ? n0 + 4 * (it % nc4) : 0;
+      acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int j0 = 0; j0 < topk; j0 += kCmbMaxTopk) {
+      f32x4 v[U][kCmbMaxTopk];
+      float w[U][kCmbMaxTopk];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < kCmbMaxTopk; ++j) {
+          const bool live = t_of[u] >= 0 && j0 + j < topk;
+          const int s = live ? t_of[u] * topk + j0 + j : 0;
+          w[u][j] = live ? a.route_w[s] : 0.0f;
+          v[u][j] = __builtin_bit_cast(
+              f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                         yr, live ? ((uint32_t)s * (uint32_t)N + (uint32_t)c_of[u]) * 4u : kOOB, 0, kDeviceScope));
+        }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < kCmbMaxTopk; ++j)
+          if (j0 + j < topk)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) acc[u][c] = __builtin_fmaf(w[u][j], v[u][j][c], acc[u][c]);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (t_of[u] >= 0)
+        __builtin_nontemporal_store(acc[u], reinterpret_cast<f32x4*>(a.out + (size_t)t_of[u] * N + c_of[u]));
+  }
+}
+
 // One output tile: rows [m0, m0 + rows_valid) of x (dense) or the gathered rows
 // s_xrow[] (MoE), columns [n0, n0 + BN) of W.
 //
@@ -225,7 +317,7 @@ constexpr int kSchedDSWrite = 0x200;
 //   (kt+1)&1) interleaved between them
 //   wait for the activation DMA and the LDS writes, then barrier
 // FULL: every row of the tile is valid, so no MFMA is skipped (branch-free body).
-template <int FMT, int BM, int BN, int WM, int WN, bool MOE, bool FULL, int XS, bool SWI>
+template <int FMT, int BM, int BN, int WM, int WN, bool MOE, bool FULL, int XS, bool SWI, bool CMB>
 __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __restrict__ wq,
                                           const uint16_t* __restrict__ sc, int m0, int n0,
                                           int rows_valid, const int* __restrict__ s_xrow,
@@ -233,6 +325,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
                                           int ks0, int nsteps, float* __restrict__ yout) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, MOE, XS>;
   static_assert(!SWI || MOE, "the fused SwiGLU epilogue is a MoE gate/up epilogue");
+  static_assert(!CMB || (MOE && !SWI), "the fused combine is a MoE down-projection epilogue");
   constexpr int kUnitsPerChunk = (FMT == kQ8) ? 2 : 4;        // 16-byte LDS writes per 16-byte load
   constexpr int kUnits = KT::kWChunks * kUnitsPerChunk;        // per thread per K step
   constexpr int kWD = (FMT == kQ4) ? 3 : 2;                    // weight prefetch distance (K steps)
@@ -360,28 +453,6 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
     }
   };
-
-  // L2 prefetch of the gathered activation rows two steps ahead (MoE ping-pong DMA waves): DMA wave
-  // xw touches the 128-byte row segment of tile rows xw * BM / 4 + lane with one 4-byte LDS-DMA
-  // load, so that the segment is in L2 by the time the real DMA of that step is issued, one step
-  // later. The LDS target is st.x[2], a 256-byte array no other access reads or writes (64 lanes
-  // x 4 bytes): every wave's prefetch overwrites it, so the load's only effect is the fetch. (A
-  // load into a register folded into a sink a step later was slower through the registers it holds.)
-  constexpr bool XPF = PP && MOE && QG_XPREFETCH;   // dense rows are contiguous: no gain measured there
-  uint32_t pfoff = kOOB;
-  if constexpr (XPF) {
-    constexpr int kRowsPerWave = BM / 4;
-    const int r = xw * kRowsPerWave + lane;
-    if (lane < kRowsPerWave && r < rows_valid) {
-      const int src = MOE ? s_xrow[r] : r;
-      if (src >= 0) pfoff = (uint32_t)src * (uint32_t)K * 2u;
-    }
-  }
-  auto prefetch_x = [&](int kt_local) {
-    const uint32_t off = (pfoff == kOOB || kt_local >= nk) ? kOOB : pfoff + (uint32_t)(ks0 + kt_local) * (uint32_t)kRowBytes;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)st.x[2], 4, off, 0, 0, 0);
-  };
-  constexpr int kPF = XPF ? 1 : 0;   // prefetch loads per DMA-wave step
 
   // weight register sets: the loads of step k are issued kWD steps ahead, into set k % kWD
   uint4 wv[kWD][WC];
@@ -673,7 +744,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       // The activation DMA (stage last read in step kt-1) goes out in kVmemSplit groups with a
       // share of the dequantisation after each, so the wave works while its loads queue in the
       // address unit. The vector-memory order is unchanged: all DMA groups, then the weight
-      // loads, then the prefetch (the wait at the end of the step counts the loads after the DMA).
+      // loads (the wait at the end of the step counts the loads after the DMA).
       constexpr int G = kVmemSplit > 0 ? kVmemSplit : 1;
 #pragma unroll
       for (int g = 0; g < G; ++g) {
@@ -682,10 +753,6 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
         if (g == G - 1) {
           issue_w(kt + kWD, wv[wset_issue], sv[wset_issue], CD);
           __builtin_amdgcn_sched_barrier(0);
-          if constexpr (XPF) {
-            prefetch_x(kt + 2);
-            __builtin_amdgcn_sched_barrier(0);
-          }
         }
         if constexpr (kVmemSplit > 0) {
 #pragma unroll
@@ -704,8 +771,8 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       mfma_phase(xs_cur, ws_cur, true);
       // this wave's activation DMA of step kt+1: the only vector-memory loads issued after it are
       // its weight loads of step kt+kWD, counted only when live (loads of steps past the last one
-      // may be deleted, and an undercount only makes the wait stricter), and its prefetch load
-      if (kt + kWD <= nk) wait_vmcnt_lgkm0<2 * CD + kPF>(); else wait_vmcnt_lgkm0<0>();
+      // may be deleted, and an undercount only makes the wait stricter)
+      if (kt + kWD <= nk) wait_vmcnt_lgkm0<2 * CD>(); else wait_vmcnt_lgkm0<0>();
       __builtin_amdgcn_s_barrier();
     };
     int kt = 0;
@@ -808,6 +875,23 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     return;
   }
   const bool full_cols = n0 + BN <= N;
+  // fused combine: per-slot rows leave with device-scope stores (32-bit offsets: the host checks
+  // that y spans less than 4 GiB)
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(yout, CMB ? (uint32_t)((size_t)a.M * (size_t)N * 4u) : 0u);
+  auto store_row4 = [&](int dst, int col, const f32x4& v) {
+    if constexpr (CMB)
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), yr, ((uint32_t)dst * (uint32_t)N + (uint32_t)col) * 4u,
+                                             0, kDeviceScope);
+    else
+      *reinterpret_cast<f32x4*>(yout + (size_t)dst * N + col) = v;
+  };
+  auto store_one = [&](int dst, int col, float v) {
+    if constexpr (CMB)
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), yr,
+                                            ((uint32_t)dst * (uint32_t)N + (uint32_t)col) * 4u, 0, kDeviceScope);
+    else
+      yout[(size_t)dst * N + col] = v;
+  };
   if (full_cols && (N & 3) == 0) {
     // Row-contiguous stores through LDS: each 32x32 accumulator block goes to a per-wave LDS
     // scratch (row stride 40 floats: the two row halves a store instruction writes fall in
@@ -842,45 +926,41 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
           if (!FULL && trow >= rows_valid) continue;
           const int dst = MOE ? s_yrow[trow] : (m0 + trow);
           if (MOE && dst < 0) continue;
-          *reinterpret_cast<f32x4*>(yout + (size_t)dst * N + col) = v;
+          store_row4(dst, col, v);
         }
       }
     }
-    return;
-  }
+  } else {
 #pragma unroll
-  for (int i = 0; i < KT::kTM; ++i) {
-    if (!FULL && i >= mblocks) continue;
+    for (int i = 0; i < KT::kTM; ++i) {
+      if (!FULL && i >= mblocks) continue;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = (i * WM + wm) * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
-      if (!FULL && row >= rows_valid) continue;
-      const int dst = MOE ? s_yrow[row] : (m0 + row);
-      if (MOE && dst < 0) continue;
-      float* yrow = yout + (size_t)dst * N + n0 + wn * KT::kWTN + lr;
-      if (full_cols) {
-#pragma unroll
-        for (int j = 0; j < KT::kTN; ++j) yrow[j * 32] = acc[i][j][r];
-      } else {
+      for (int r = 0; r < 16; ++r) {
+        const int row = (i * WM + wm) * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+        if (!FULL && row >= rows_valid) continue;
+        const int dst = MOE ? s_yrow[row] : (m0 + row);
+        if (MOE && dst < 0) continue;
+        const int col0 = n0 + wn * KT::kWTN + lr;
 #pragma unroll
         for (int j = 0; j < KT::kTN; ++j)
-          if (n0 + wn * KT::kWTN + j * 32 + lr < N) yrow[j * 32] = acc[i][j][r];
+          if (full_cols || col0 + j * 32 < N) store_one(dst, col0 + j * 32, acc[i][j][r]);
       }
     }
   }
+  if constexpr (CMB) combine_arrivals<KT::kThreads, BM, BN>(a, yr, s_yrow, rows_valid, n0, st);
 }
 
-template <int FMT, int BM, int BN, int WM, int WN, bool MOE, int XS, bool SWI>
+template <int FMT, int BM, int BN, int WM, int WN, bool MOE, int XS, bool SWI, bool CMB = false>
 __device__ __forceinline__ void tile_dispatch(const TileArgs& a, const uint8_t* __restrict__ wq,
                                               const uint16_t* __restrict__ sc, int m0, int n0, int rows_valid,
                                               const int* __restrict__ s_xrow, const int* __restrict__ s_yrow,
                                               LdsStages lds, int ks0, int nsteps, float* __restrict__ yout) {
   if (rows_valid == BM)
-    tile_body<FMT, BM, BN, WM, WN, MOE, true, XS, SWI>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0, nsteps,
-                                                       yout);
+    tile_body<FMT, BM, BN, WM, WN, MOE, true, XS, SWI, CMB>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0,
+                                                            nsteps, yout);
   else
-    tile_body<FMT, BM, BN, WM, WN, MOE, false, XS, SWI>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0, nsteps,
-                                                        yout);
+    tile_body<FMT, BM, BN, WM, WN, MOE, false, XS, SWI, CMB>(a, wq, sc, m0, n0, rows_valid, s_xrow, s_yrow, lds, ks0,
+                                                             nsteps, yout);
 }
 
 template <int FMT, int BM, int BN, int WM, int WN, int XS>
@@ -889,10 +969,10 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
   using KT = TileKernel<FMT, BM, BN, WM, WN, false, XS>;
   __shared__ __attribute__((aligned(1024))) char lx0[KT::kXTileBytes];
   __shared__ __attribute__((aligned(1024))) char lx1[KT::kXTileBytes];
-  __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 256];
+  __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 16];
   __shared__ __attribute__((aligned(1024))) char lw0[KT::kWTileBytes];
   __shared__ __attribute__((aligned(1024))) char lw1[KT::kWTileBytes];
-  const LdsStages lds{{lx0, lx1, lx2}, {lw0, lw1}};
+  const LdsStages lds{{lx0, lx1, XS == 3 ? lx2 : nullptr}, {lw0, lw1}};
   const int mt_n = (a.M + BM - 1) / BM;
   const int nt_n = (a.N + BN - 1) / BN;
   const int ntiles = mt_n * nt_n;
@@ -916,17 +996,17 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
 // Work items are (expert, m tile, n tile) over active experts only; every
 // workgroup decodes its item from the per-expert counts, so the host never
 // needs the routing.
-template <int FMT, int BM, int BN, int WM, int WN, int XS, bool SWI>
+template <int FMT, int BM, int BN, int WM, int WN, int XS, bool SWI, bool CMB = false>
 // four-wave tiles (67 KB of LDS) run two workgroups per CU: at most 256 registers per lane
 __global__ __launch_bounds__(WM * WN * 64, WM * WN == 4 ? 2 : 1) void moe_kernel(TileArgs a, ExpertPtrs ep) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, true, XS>;
   static_assert(KT::kThreads >= kMaxExpertsPerLaunch, "the tile prefix needs one lane per expert");
   __shared__ __attribute__((aligned(1024))) char lx0[KT::kXTileBytes];
   __shared__ __attribute__((aligned(1024))) char lx1[KT::kXTileBytes];
-  __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 256];
+  __shared__ __attribute__((aligned(1024))) char lx2[XS == 3 ? KT::kXTileBytes : 16];
   __shared__ __attribute__((aligned(1024))) char lw0[KT::kWTileBytes];
   __shared__ __attribute__((aligned(1024))) char lw1[KT::kWTileBytes];
-  const LdsStages lds{{lx0, lx1, lx2}, {lw0, lw1}};
+  const LdsStages lds{{lx0, lx1, XS == 3 ? lx2 : nullptr}, {lw0, lw1}};
   __shared__ int s_prefix[kMaxExpertsPerLaunch + 1];
   __shared__ int s_rowidx[BM];   // y row (assignment) of each tile row
   __shared__ int s_xrow[BM];     // x row (token = assignment / topk) of each tile row
@@ -961,16 +1041,20 @@ __global__ __launch_bounds__(WM * WN * 64, WM * WN == 4 ? 2 : 1) void moe_kernel
   if (tid >= 64 && tid < 128) s_prefix[tid + 1] += s_wsum[0];
   __syncthreads();
   // Work unit: an m-tile group = one expert's BM gathered rows against all nt_n column tiles.
-  // Workgroups reach the 8 XCDs round-robin (bid % 8); XCD x takes groups x, x + 8, x + 16, ...
-  // with a group's column tiles consecutive, so the group's gathered rows and an expert's
-  // weights are shared through that XCD's L2, while heavy and light groups (skewed routing)
-  // spread evenly over the XCDs. The host sizes the grid as 8 * ceil(groups bound / 8) * nt_n.
+  // Workgroups reach the 8 XCDs round-robin (bid % 8). Groups are dealt to the XCDs in runs of
+  // kMoeRun consecutive groups (XCD x takes runs x, x + 8, ...), so heavy and light groups (skewed
+  // routing) spread evenly over the XCDs while the groups of one run -- mostly the same expert --
+  // share an L2. Inside a run the workgroups go column tile by column tile, the run's groups
+  // innermost: neighbouring workgroups read the same weight column tile, and each group's gathered
+  // rows serve its nt_n column tiles within a window of kMoeRun * nt_n workgroups.
+  // The host sizes the grid as 8 * kMoeRun * ceil(groups bound / (8 * kMoeRun)) * nt_n.
   const int ngroups = s_prefix[ne];
   const int xcd = (int)blockIdx.x & 7;
   const int local = (int)blockIdx.x >> 3;
-  const int gl = local / nt_n;
-  const int nt = local - gl * nt_n;
-  const int g = xcd + 8 * gl;
+  const int run = local / (kMoeRun * nt_n);
+  const int within = local - run * (kMoeRun * nt_n);
+  const int nt = within / kMoeRun;
+  const int g = (run * 8 + xcd) * kMoeRun + (within - nt * kMoeRun);
   if (g >= ngroups) return;
   // largest e with s_prefix[e] <= g
   int lo = 0, hi = ne;
@@ -993,8 +1077,8 @@ __global__ __launch_bounds__(WM * WN * 64, WM * WN == 4 ? 2 : 1) void moe_kernel
     s_xrow[r] = asg < 0 ? -1 : asg / a.topk;
   }
   __syncthreads();
-  tile_dispatch<FMT, BM, BN, WM, WN, true, XS, SWI>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow, s_rowidx,
-                                                    lds, 0, (a.K + kBK - 1) / kBK, a.y);
+  tile_dispatch<FMT, BM, BN, WM, WN, true, XS, SWI, CMB>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow,
+                                                         s_rowidx, lds, 0, (a.K + kBK - 1) / kBK, a.y);
 }
 
 }  // namespace qg

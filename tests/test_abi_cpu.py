@@ -32,7 +32,8 @@ def header_prototypes():
 
 def test_header_declares_the_boundary():
     p = header_prototypes()
-    for name in ("qgemm_dense", "qgemm_moe", "qgemm_moe_bucket", "qgemm_moe_grouped", "qgemm_moe_gate_up_swiglu", "qgemm_swiglu",
+    for name in ("qgemm_dense", "qgemm_moe", "qgemm_moe_bucket", "qgemm_moe_grouped", "qgemm_moe_gate_up_swiglu",
+                 "qgemm_moe_down_combine", "qgemm_swiglu",
                  "qgemm_moe_combine", "qgemm_attention_prefill", "qgemm_last_error", "qgemm_release", "qgemm_version"):
         assert name in p
 
@@ -93,6 +94,17 @@ def test_moe_host_validation(qmod):
     assert lib.qgemm_swiglu(16, 16, 0, 16, None) == 0
     assert lib.qgemm_moe_combine(16, 16, 16, 4, 2, 6, None) == -1
     assert lib.qgemm_moe_combine(16, 16, 16, 0, 2, 8, None) == 0
+    # fused down projection + combine: h, perm, offsets, wq, scales, route_w, y2, out, T, E, topk, N, K, fmt
+    dc = lib.qgemm_moe_down_combine
+    assert dc(16, 16, 16, ptrs, ptrs, 16, 16, 16, 4, 4, 2, 130, 64, 0, None) == -1       # N % 4
+    assert "multiple of 4" in qmod.last_error()
+    assert dc(16, 16, 16, ptrs, ptrs, 16, 16, 16, 4, 4, 5, 128, 64, 0, None) == -1       # topk > E
+    assert dc(16, 16, 16, ptrs, ptrs, 16, 16, 16, 4, 4, 2, 128, 48, 0, None) == -1       # K % 32
+    assert dc(16, 16, 16, ptrs, ptrs, 16, 16, 16, 65536, 4, 4, 4096, 64, 0, None) == -3  # y2 spans 4 GiB
+    assert "4 GiB" in qmod.last_error()
+    assert dc(16, 16, 16, ptrs, ptrs, 16, 16, 16, 0, 4, 2, 128, 64, 0, None) == 0        # T == 0
+    assert dc(16, 16, 16, ptrs, ptrs, 0, 16, 16, 4, 4, 2, 128, 64, 0, None) == -1        # null route_w
+    assert dc(16, 16, 16, ptrs, ptrs, 16, 16, 24, 4, 4, 2, 128, 64, 0, None) == -2       # out misaligned
 
 
 def test_attention_host_validation(qmod):
