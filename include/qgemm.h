@@ -109,6 +109,27 @@ int qgemm_moe(const void* x, const int32_t* token_expert_idx,
               int N, int K, int fmt, hipStream_t stream);
 
 /*
+ * qgemm_moe for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments, results bitwise equal to qgemm_moe, and no hipMalloc, hipFree
+ * or other allocation on any call. The bucketing buffers (permutation,
+ * per-block expert histograms, error flag) live in a static device array of
+ * 2 MiB + 256 bytes that each device holds until the process ends; the first
+ * call on a device looks up its address there. Limits: T*topk <= 262144 and
+ * ceil-blocks(T*topk) * E <= 262144 (the bucketing uses blocks of 512 slots,
+ * at most 1024 blocks); larger problems return QGEMM_EUNSUPPORTED before
+ * anything is enqueued. Every call on a device shares that device's array and
+ * leaves its contents behind: calls that can overlap on one device (other
+ * streams, other host threads) race and must be ordered by the caller.
+ * QGEMM_VALIDATE is not consulted (the call never synchronises); inconsistent
+ * routing tables still give NaN rows as for qgemm_moe.
+ */
+int qgemm_moe_noalloc(const void* x, const int32_t* token_expert_idx,
+                      const int32_t* expert_offsets, const void* const* wq,
+                      const void* const* scales, float* y, int T, int E, int topk,
+                      int N, int K, int fmt, hipStream_t stream);
+
+/*
  * The two halves of qgemm_moe, for callers that keep their own bucketing
  * buffer (the MoE expert GEMM of Section 3.1 needs each expert's routed
  * token list).

@@ -15,7 +15,7 @@ import os
 
 import torch  # imported before the library so that both share one HIP runtime
 
-__all__ = ["Q8", "Q4", "QGemmError", "lib", "lib_path", "dense", "moe", "moe_bucket", "moe_grouped",
+__all__ = ["Q8", "Q4", "QGemmError", "lib", "lib_path", "dense", "moe", "moe_noalloc", "moe_bucket", "moe_grouped",
            "moe_gate_up_swiglu", "moe_down_combine", "swiglu", "moe_combine", "attention_prefill", "probe_mfma_clock", "last_error", "release", "version", "EXPORTS", "ExpertTable"]
 
 Q8 = 0
@@ -29,6 +29,7 @@ _i = ctypes.c_int
 EXPORTS = {
     "qgemm_dense": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp]),
     "qgemm_moe": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "qgemm_moe_noalloc": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "qgemm_moe_bucket": (_i, [_vp, _vp, _vp, _i, _i, _vp]),
     "qgemm_moe_grouped": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "qgemm_moe_gate_up_swiglu": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
@@ -201,6 +202,27 @@ def moe(x, token_expert_idx, expert_offsets, wq, scales, topk: int, fmt: int, ou
     _need(out, "out", (torch.float32,), 2)
     _check(lib().qgemm_moe(x.data_ptr(), token_expert_idx.data_ptr(), expert_offsets.data_ptr(), wp, sp,
                            out.data_ptr(), T, E, topk, N, K, fmt, _stream(x)))
+    return out
+
+
+def moe_noalloc(x, token_expert_idx, expert_offsets, wq, scales, topk: int, fmt: int, out=None):
+    """``qgemm_moe_noalloc``: as ``moe`` with the bucketing buffers in the library's static device
+    scratch (no device allocation in the call; ``out`` should be given by callers that cannot
+    allocate). ``wq`` may be an ExpertTable."""
+    _need(x, "x", (torch.bfloat16,), 2)
+    _need(token_expert_idx, "token_expert_idx", (torch.int32,), 1)
+    _need(expert_offsets, "expert_offsets", (torch.int32,), 1)
+    T, K = x.shape
+    E = expert_offsets.shape[0] - 1
+    wq, scales, wp, sp = _expert_tables(wq, scales, E)
+    N = wq[0].shape[0]
+    if token_expert_idx.shape[0] != T * topk:
+        raise ValueError("token_expert_idx must have T*topk entries")
+    if out is None:
+        out = torch.empty((T * topk, N), dtype=torch.float32, device=x.device)
+    _need(out, "out", (torch.float32,), 2)
+    _check(lib().qgemm_moe_noalloc(x.data_ptr(), token_expert_idx.data_ptr(), expert_offsets.data_ptr(), wp, sp,
+                                   out.data_ptr(), T, E, topk, N, K, fmt, _stream(x)))
     return out
 
 

@@ -18,6 +18,12 @@
 #include "qgemm_smallm.hpp"
 #include "attn_kernels.hpp"
 
+// Scratch of qgemm_moe_noalloc (2 MiB + 256 bytes per device, held until the process ends): the
+// token-slot permutation, the per-block expert histograms and the error flag. In host code this
+// name is only a stand-in for the symbol; kernels get the per-device address from
+// hipGetSymbolAddress.
+static __device__ __align__(256) int32_t scratch[(1 << 18) + (1 << 18) + 64];
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -321,6 +327,19 @@ int moe_args_check(const void* x, const void* idx_or_perm, const int32_t* offset
   return QGEMM_OK;
 }
 
+// ---------------------------------------------------------------------------
+// allocation-free MoE entry point: the bucketing buffers live in a static device array
+// ---------------------------------------------------------------------------
+
+constexpr int kNoAllocMaxSlots = 1 << 18;    // token slots (T * topk): the permutation
+constexpr int kNoAllocMaxCounts = 1 << 18;   // per-block expert histograms (blocks x E)
+constexpr int kNoAllocFlag = kNoAllocMaxSlots + kNoAllocMaxCounts;   // error flag (sequence number)
+constexpr int kMaxDevices = 64;
+
+std::mutex g_scratch_mutex;
+int32_t* g_scratch_dev[kMaxDevices] = {};    // device address of `scratch` on each device
+int g_scratch_seq[kMaxDevices] = {};
+
 bool validate_env() {
   const char* v = getenv("QGEMM_VALIDATE");
   return v != nullptr && v[0] == '1';
@@ -540,6 +559,67 @@ int qgemm_moe_down_combine(const void* h, const int32_t* perm, const int32_t* ex
   a.counters = ctr;
   rc = (fmt == QGEMM_Q8) ? launch_moe<qg::kQ8, false, true>(a, wq, scales, E, stream)
                          : launch_moe<qg::kQ4, false, true>(a, wq, scales, E, stream);
+  return rc == QGEMM_OK ? ok() : rc;
+}
+
+int qgemm_moe_noalloc(const void* x, const int32_t* token_expert_idx, const int32_t* expert_offsets,
+                      const void* const* wq, const void* const* scales, float* y, int T, int E, int topk, int N,
+                      int K, int fmt, hipStream_t stream) {
+  int rc = moe_args_check(x, token_expert_idx, expert_offsets, wq, scales, y, T, E, topk, N, K, fmt);
+  if (rc != QGEMM_OK || T == 0) return rc == QGEMM_OK ? ok() : rc;
+  const int n = T * topk;
+  int chunk, nblk;
+  bucket_geometry(n, &chunk, &nblk);
+  if (n > kNoAllocMaxSlots)
+    return fail(QGEMM_EUNSUPPORTED, "qgemm_moe_noalloc: T*topk = %d exceeds the static scratch (%d token slots)", n,
+                kNoAllocMaxSlots);
+  if ((long)nblk * E > kNoAllocMaxCounts)
+    return fail(QGEMM_EUNSUPPORTED,
+                "qgemm_moe_noalloc: %d bucketing blocks x %d experts exceed the static scratch (%d counts)", nblk, E,
+                kNoAllocMaxCounts);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(QGEMM_EHIP, "hipGetDevice failed");
+  }
+  if (dev < 0 || dev >= kMaxDevices) return fail(QGEMM_EUNSUPPORTED, "device %d beyond the supported %d", dev, kMaxDevices);
+  int32_t* base;
+  int seq;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_dev[dev] == nullptr) {
+      // once per device, with that device current: the address of this device's copy of the array
+      void* p = nullptr;
+      const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || p == nullptr) {
+        (void)hipGetLastError();
+        return fail(QGEMM_EHIP, "hipGetSymbolAddress of the static scratch failed: %s", hipGetErrorString(e));
+      }
+      g_scratch_dev[dev] = static_cast<int32_t*>(p);
+    }
+    base = g_scratch_dev[dev];
+    g_scratch_seq[dev] = g_scratch_seq[dev] == 0x7fffffff ? 1 : g_scratch_seq[dev] + 1;
+    seq = g_scratch_seq[dev];
+  }
+  int32_t* perm = base;
+  int32_t* counts = base + kNoAllocMaxSlots;
+  int32_t* flag = base + kNoAllocFlag;
+  (void)hipGetLastError();
+  // every entry of perm and of the histograms is written by the bucketing kernels before it is
+  // read; the flag is compared with this call's sequence number, so nothing needs clearing
+  rc = enqueue_bucket(token_expert_idx, expert_offsets, perm, n, E, counts, flag, seq, y, N, stream);
+  if (rc != QGEMM_OK) return rc;
+  qg::TileArgs a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.y = y;
+  a.M = n;
+  a.N = N;
+  a.K = K;
+  a.perm = perm;
+  a.offsets = expert_offsets;
+  a.topk = topk;
+  a.T = T;
+  rc = (fmt == QGEMM_Q8) ? launch_moe<qg::kQ8>(a, wq, scales, E, stream) : launch_moe<qg::kQ4>(a, wq, scales, E, stream);
   return rc == QGEMM_OK ? ok() : rc;
 }
 
