@@ -213,20 +213,23 @@ int launch_moe_cfg(qg::TileArgs a, const void* const* wq, const void* const* sc,
   return QGEMM_OK;
 }
 
-// Tile from the mean rows per expert (the host does not see the routing): groups of about
-// 100-200 rows fit one 192-row tile each; larger groups use 256-row tiles. Short prompts (at
-// most 32 rows per expert on average) use 128x128 tiles of four waves, two workgroups per CU:
-// twice the workgroups of the 256-wide tiles over the few active experts' weights, so the
-// CUs fill (measured at T=128, E=128, top-8: gate/up + SiLU 66.5 against 73 us, down 31
-// against 34 us; at T=2048 the same tile is slower, 196 against 159 us and 125 against 108 us).
 // Column tile width of the configuration launch_moe picks (the fused combine counts arrivals per
 // (token, column tile)).
 inline int moe_tile_bn(long M, int E) { return (M / E) <= 32 ? 128 : 256; }
 
+// Tile from the mean rows per expert (the host does not see the routing): groups of about
+// 100-200 rows fit one 192-row tile each; larger groups use 256-row tiles. Short prompts (at
+// most 32 rows per expert on average) use four-wave tiles with 128 columns: twice the
+// workgroups of the 256-wide tiles over the few active experts' weights, so the CUs fill
+// (measured at T=128, E=128, top-8: gate/up + SiLU 66.5 against 73 us, down 31 against 34 us;
+// at T=2048 the same tile is slower, 196 against 159 us and 125 against 108 us). The fused
+// gate/up tile is 64 rows high there (three workgroups per CU, so the whole launch runs in one
+// round: 52-53 against 67-68 us); the plain tile stays 128 rows high (down 31-33 against 33-34 us
+// with 64 rows).
 template <int FMT, bool SWI = false, bool CMB = false>
 int launch_moe(qg::TileArgs a, const void* const* wq, const void* const* sc, int E, hipStream_t s) {
   const long mean_rows = (long)a.M / E;
-  if (mean_rows <= 32) return launch_moe_cfg<FMT, 128, 128, 2, 2, 2, SWI, CMB>(a, wq, sc, E, s);
+  if (mean_rows <= 32) return launch_moe_cfg<FMT, SWI ? 64 : 128, 128, 2, 2, 2, SWI, CMB>(a, wq, sc, E, s);
   if (mean_rows > 192) return launch_moe_cfg<FMT, 256, 256, 2, 4, 2, SWI, CMB>(a, wq, sc, E, s);
   return launch_moe_cfg<FMT, 192, 256, 2, 4, 2, SWI, CMB>(a, wq, sc, E, s);
 }

@@ -116,6 +116,7 @@ __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (
 #define QG_PINGPONG 1
 #endif
 
+
 // Groups the ping-pong DMA-role step splits its activation DMA into, each followed by a share of
 // its dequantisation (0: all loads first, then all dequantisation)
 #ifndef QG_VMEM_SPLIT
@@ -369,6 +370,8 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   const bool isD = PP ? wm == 1 : true;            // issues activation DMA
   const bool isQ = PP ? wm == 0 : true;            // loads and dequantises weights
   const int xw = PP ? (isD ? wave - WN : 0) : wave;  // DMA wave index within its role
+  // 8-row group of the tile fetched by DMA load j of this wave
+  auto xgroup = [&](int j) { return xw * XL + j; };
   // first weight chunk of this thread: dequant threads t take chunks t + i * stride (i < CQ), DMA
   // threads t' take CQ * stride + t' + i * stride (i < CD)
   const int wt = PP ? (isQ ? tid : CQ * (KT::kThreads / 2) + (tid - KT::kThreads / 2)) : tid;
@@ -379,14 +382,14 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   int dma_c[XL];
 #pragma unroll
   for (int j = 0; j < XL; ++j) {
-    const int r = (xw * XL + j) * 8 + (lane >> 3);
+    const int r = xgroup(j) * 8 + (lane >> 3);
     dma_c[j] = (lane & 7) ^ row_swizzle(r);     // the chunk that lds_chunk(r, .) places at slot lane & 7
   }
   if constexpr (MOE) {
     xr = make_rsrc(a.x, (uint32_t)a.T * (uint32_t)K * 2u);
 #pragma unroll
     for (int j = 0; j < XL; ++j) {
-      const int r = (xw * XL + j) * 8 + (lane >> 3);
+      const int r = xgroup(j) * 8 + (lane >> 3);
       const int src = (r < rows_valid) ? s_xrow[r] : -1;
       xoff[j] = (src >= 0) ? (uint32_t)src * (uint32_t)K * 2u + (uint32_t)dma_c[j] * 16u : kOOB;
     }
@@ -394,7 +397,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     xr = make_rsrc(a.x + (size_t)m0 * K, (uint32_t)rows_valid * (uint32_t)K * 2u);
 #pragma unroll
     for (int j = 0; j < XL; ++j) {
-      const int r = (xw * XL + j) * 8 + (lane >> 3);
+      const int r = xgroup(j) * 8 + (lane >> 3);
       xoff[j] = (uint32_t)r * (uint32_t)K * 2u + (uint32_t)dma_c[j] * 16u;
     }
   }
@@ -446,10 +449,10 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
       // an 8-row group wholly past the valid rows is not fetched at all: its LDS rows keep
       // stale data, which only reaches accumulator rows that are never stored. (With three
       // stages the waits count this step's activation loads, so every group is issued.)
-      if (!FULL && XS == 2 && (xw * XL + j) * 8 >= rows_valid) continue;
+      if (!FULL && XS == 2 && xgroup(j) * 8 >= rows_valid) continue;
       uint32_t off = (xoff[j] == kOOB) ? kOOB : xoff[j] + kbyte;
       if (tail && (kt_local >= nk || kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
-      lds_char* dst = xstage_ptr(stage) + (xw * XL + j) * 1024;
+      lds_char* dst = xstage_ptr(stage) + xgroup(j) * 1024;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
     }
   };
@@ -809,8 +812,12 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     if ((swi_inter & 7) == 0 && h0 + (wn + 1) * kHW <= swi_inter) {
       constexpr int kStrideH = kHW + 8;           // bf16 per scratch row (16-byte aligned rows)
       constexpr int kHalf = KT::kWaves / 2;
-      static_assert(kHalf * 32 * kStrideH * 2 <= KT::kXTileBytes, "epilogue scratch must fit an activation stage");
-      lds_char* scratch = xstage_ptr(wave / kHalf) + (wave % kHalf) * (32 * kStrideH * 2);
+      // half of the waves per LDS stage: the activation stages, or the weight stages when an
+      // activation stage is too small (short tiles)
+      constexpr int kNeed = kHalf * 32 * kStrideH * 2;
+      constexpr bool kInX = kNeed <= KT::kXTileBytes;
+      static_assert(kInX || kNeed <= KT::kWTileBytes, "epilogue scratch must fit an LDS stage");
+      lds_char* scratch = (kInX ? xstage_ptr(wave / kHalf) : wstage_ptr(wave / kHalf)) + (wave % kHalf) * (32 * kStrideH * 2);
       constexpr int kChunksRow = kHW / 8;
 #pragma unroll
       for (int i = 0; i < KT::kTM; ++i) {
@@ -900,8 +907,10 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     // K loop (the loop ends with a barrier after the last fragment reads and DMA waits).
     constexpr int kStride = 40;
     constexpr int kHalf = KT::kWaves / 2;
-    static_assert(kHalf * 32 * kStride * 4 <= KT::kXTileBytes, "epilogue scratch must fit an activation stage");
-    lds_char* scratch = xstage_ptr(wave / kHalf) + (wave % kHalf) * (32 * kStride * 4);
+    constexpr int kNeed = kHalf * 32 * kStride * 4;
+    constexpr bool kInX = kNeed <= KT::kXTileBytes;
+    static_assert(kInX || kNeed <= KT::kWTileBytes, "epilogue scratch must fit an LDS stage");
+    lds_char* scratch = (kInX ? xstage_ptr(wave / kHalf) : wstage_ptr(wave / kHalf)) + (wave % kHalf) * (32 * kStride * 4);
     const int rr = lane >> 3;                 // row within an 8-row read group
     const int cc = (lane & 7) * 4;            // first of this lane's 4 columns
 #pragma unroll
@@ -997,8 +1006,10 @@ __global__ __launch_bounds__(WM * WN * 64) void dense_kernel(TileArgs a, const u
 // workgroup decodes its item from the per-expert counts, so the host never
 // needs the routing.
 template <int FMT, int BM, int BN, int WM, int WN, int XS, bool SWI, bool CMB = false>
-// four-wave tiles (67 KB of LDS) run two workgroups per CU: at most 256 registers per lane
-__global__ __launch_bounds__(WM * WN * 64, WM * WN == 4 ? 2 : 1) void moe_kernel(TileArgs a, ExpertPtrs ep) {
+// four-wave 128x128 tiles (67 KB of LDS) run two workgroups per CU (at most 256 registers per
+// lane), four-wave 64x128 tiles (50 KB) three
+__global__ __launch_bounds__(WM * WN * 64, WM * WN == 4 ? (BM <= 64 ? 3 : 2) : 1) void moe_kernel(TileArgs a,
+                                                                                                  ExpertPtrs ep) {
   using KT = TileKernel<FMT, BM, BN, WM, WN, true, XS>;
   static_assert(KT::kThreads >= kMaxExpertsPerLaunch, "the tile prefix needs one lane per expert");
   __shared__ __attribute__((aligned(1024))) char lx0[KT::kXTileBytes];
