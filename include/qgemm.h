@@ -74,8 +74,12 @@ enum qgemm_status {
  * regime of Section 2.3 and the batched verification of Section 5.2) takes a
  * separate bandwidth-oriented kernel: weights dequantised straight into
  * matrix-core registers, K split over waves (and over workgroups when N is
- * small, through the same workspace); its results are bitwise reproducible
- * but not bitwise equal to the M > 16 kernels (another summation order).
+ * small, through the same workspace). The same kernel, in blocks of 16
+ * activation rows, serves 16 < M <= 128 when ceil(N/128) times the number of
+ * 16-row blocks (rounded up to 2, 4 or 8) is at most 512: short prompts whose
+ * few 128x128 output tiles would leave most CUs idle. Its results are bitwise
+ * reproducible but not bitwise equal to the tile kernels' (another summation
+ * order).
  */
 int qgemm_dense(const void* x, const void* wq, const void* scales, float* y,
                 int M, int N, int K, int fmt, hipStream_t stream);

@@ -101,22 +101,38 @@ constexpr int kMinStepsPerSplit = 12;
 constexpr long kSmTargetGroups = 256;   // workgroups (of eight waves) to fill the CUs without a K split
 constexpr int kSmMaxJW = 8;             // chunks per wave held in registers
 
-template <int FMT, int JW>
+template <int FMT, int JW, int MT>
 int launch_small(const qg::SmallArgs& a, long groups, hipStream_t s) {
-  hipLaunchKernelGGL((qg::smallm_kernel<FMT, JW, qg::kSmWaves>), dim3((unsigned)groups), dim3(qg::kSmWaves * 64),
+  hipLaunchKernelGGL((qg::smallm_kernel<FMT, JW, qg::kSmWaves, MT>), dim3((unsigned)groups), dim3(qg::kSmWaves * 64),
                      qg::smallm_scale_lds_bytes(a.nbp_log2), s, a);
   return check_launch("qgemm_dense (small M)");
 }
 
-// M <= 16: 32 weight rows per workgroup; K is split over workgroups only when there are fewer
-// than kSmTargetGroups row blocks (or a wave would hold more than kSmMaxJW chunks). Split
-// partials go to the split-K workspace and a second kernel adds them in split order.
+template <int FMT, int MT>
+int launch_small_jw(const qg::SmallArgs& a, int JW, long groups, hipStream_t s) {
+  switch (JW) {
+    case 1: return launch_small<FMT, 1, MT>(a, groups, s);
+    case 2: return launch_small<FMT, 2, MT>(a, groups, s);
+    case 4: return launch_small<FMT, 4, MT>(a, groups, s);
+    default: return launch_small<FMT, 8, MT>(a, groups, s);
+  }
+}
+
+// M <= 16 (or up to 128 in MT blocks of 16 columns): 32 weight rows per workgroup; K is split
+// over workgroups only when there are fewer than 256 row blocks (or a wave would hold more than
+// kSmMaxJW chunks). With several column blocks the call is latency-bound rather than
+// weight-streaming, and a split keeps at least 4 chunks per workgroup (measured on the split
+// targets 32 / 64 / 128 / 256: 128x1024x1024 Q8 11.0 / 9.6 / 9.5 / 10.5 us, 128x2048x8192 Q8
+// 38 / 38 / 38 / 24 us, 96x2048x768 Q4 9.2 / 9.2 / 10.3 / 10.4 us; this rule picks the best of
+// each). Split partials go to the split-K workspace and a second kernel adds them in split order.
 template <int FMT>
 int small_dispatch(const qg::TileArgs& t, const void* wq, const void* sc, hipStream_t s) {
   using F = qg::SmallFmt<FMT>;
+  const int MT = t.M <= 16 ? 1 : t.M <= 32 ? 2 : t.M <= 64 ? 4 : 8;
   const long nc = (t.K + F::kKC - 1) / F::kKC;
   const long P = (t.N + qg::kSmRows - 1) / qg::kSmRows;
   long S = std::min<long>(nc, (kSmTargetGroups + P - 1) / P);
+  if (MT > 1) S = std::min<long>(S, std::max<long>(1, nc / 4));
   S = std::max<long>(S, (nc + qg::kSmWaves * kSmMaxJW - 1) / (qg::kSmWaves * kSmMaxJW));
   const long cps = (nc + S - 1) / S;
   S = (nc + cps - 1) / cps;
@@ -144,11 +160,11 @@ int small_dispatch(const qg::TileArgs& t, const void* wq, const void* sc, hipStr
     if (rc != QGEMM_OK) return rc;
   }
   int rc;
-  switch (JW) {
-    case 1: rc = launch_small<FMT, 1>(a, P * S, s); break;
-    case 2: rc = launch_small<FMT, 2>(a, P * S, s); break;
-    case 4: rc = launch_small<FMT, 4>(a, P * S, s); break;
-    default: rc = launch_small<FMT, 8>(a, P * S, s); break;
+  switch (MT) {
+    case 1: rc = launch_small_jw<FMT, 1>(a, JW, P * S, s); break;
+    case 2: rc = launch_small_jw<FMT, 2>(a, JW, P * S, s); break;
+    case 4: rc = launch_small_jw<FMT, 4>(a, JW, P * S, s); break;
+    default: rc = launch_small_jw<FMT, 8>(a, JW, P * S, s); break;
   }
   if (rc != QGEMM_OK || S == 1) return rc;
   hipLaunchKernelGGL(qg::smallm_reduce_kernel, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, s, a.ws, a.y,
@@ -159,6 +175,15 @@ int small_dispatch(const qg::TileArgs& t, const void* wq, const void* sc, hipStr
 template <int FMT>
 int dense_dispatch(qg::TileArgs a, const void* wq, const void* sc, hipStream_t s) {
   if (a.M <= qg::kSmMaxM) return small_dispatch<FMT>(a, wq, sc, s);
+  // up to 128 rows, when the 128x128 tiles would occupy few CUs (each walking the whole K range
+  // alone), the small-M kernel with MT blocks of 16 activation columns spreads K over waves; its
+  // cost grows with MT, so it takes over while (128-wide column tiles) x MT <= 512 (measured:
+  // 128x8192x2048 Q8 20.6 against 29.1 us with the tiles, 64x14336x4096 Q4 40 against 60 us,
+  // 17x8192x2048 Q8 7.5 against 32.6 us; 128x16384x2048 Q8 39 against 31 us stays on the tiles)
+  if (a.M <= qg::kSmMaxM * qg::kSmMaxMT) {
+    const int MT = a.M <= 32 ? 2 : a.M <= 64 ? 4 : 8;
+    if ((long)((a.N + 127) / 128) * MT <= 512) return small_dispatch<FMT>(a, wq, sc, s);
+  }
   a.splits = 1;
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
   if (a.M >= 256 && a.N >= 256 && big >= 200) return launch_dense<FMT, 256, 256, 2, 4, 2>(a, wq, sc, s);

@@ -1,6 +1,7 @@
-// Small-M dense GEMM (at most 16 activation rows): the shape of decode and of batched
-// speculative-draft verification, which the paper names as the memory-bound side of inference
-// (Section 2.3) and as future work for its matrix-unit kernels (Section 5.2). Every packed weight
+// Small-M dense GEMM (at most 16 activation rows, or up to 128 in blocks of 16): the shape of
+// decode and of batched speculative-draft verification, which the paper names as the
+// memory-bound side of inference (Section 2.3) and as future work for its matrix-unit kernels
+// (Section 5.2), and of short prompts whose few output tiles would leave most CUs idle. Every packed weight
 // is read once and the arithmetic per weight byte is tiny, so the call is bound by HBM bandwidth:
 // there is no LDS staging of the weights. Each lane dequantises its own 16-byte weight load
 // straight into MFMA operand registers (v_mfma_f32_16x16x32_bf16, weights as the 16-row A
@@ -18,7 +19,8 @@
 // consecutive scales (a few cache lines per load instead of one line per row) and handed to
 // the lanes that use them through LDS.
 // Partial sums are combined in a fixed order: chunks in increasing order inside a wave, waves
-// 0..WAVES-1 through LDS, then (when K is split over workgroups) splits 0..S-1 by a second kernel.
+// 0..WAVES-1 through LDS (each output piece added up by one wave), then (when K is split over
+// workgroups) splits 0..S-1 by a second kernel.
 // Results are therefore bitwise reproducible.
 #pragma once
 
@@ -27,7 +29,8 @@
 namespace qg {
 
 constexpr int kSmRows = 32;       // weight rows per workgroup: two 16-row MFMA groups per wave
-constexpr int kSmMaxM = 16;       // activation rows = MFMA B columns
+constexpr int kSmMaxM = 16;       // activation rows of one MFMA B operand (16 columns)
+constexpr int kSmMaxMT = 8;       // 16-column activation blocks per call at most (M <= 128)
 constexpr int kSmWaves = 8;       // waves per workgroup
 // chunks of a wave in flight: three for Q8, two for Q4, whose four dequantisation units per
 // load make the VALU work of a chunk twice as long (measured on MI355X at M = 1, 4, 16: Q8 three
@@ -66,7 +69,9 @@ __host__ __device__ constexpr int smallm_scale_lds_bytes(int nbp_log2) {
 
 // JW: chunks per wave held in registers (the host keeps ceil(cps / WAVES) <= JW and
 // cps * blocks per chunk <= 2^nbp_log2 <= JW * WAVES * blocks per chunk).
-template <int FMT, int JW, int WAVES>
+// MT: 16-column blocks of activation rows (M <= 16 MT): every dequantised weight operand feeds
+// MT MFMAs, one per block, so a weight is still read and dequantised once per call.
+template <int FMT, int JW, int WAVES, int MT = 1>
 __global__ __launch_bounds__(WAVES * 64) void smallm_kernel(SmallArgs a) {
   using F = SmallFmt<FMT>;
   constexpr int KC = F::kKC;
@@ -75,7 +80,7 @@ __global__ __launch_bounds__(WAVES * 64) void smallm_kernel(SmallArgs a) {
   constexpr int T = WAVES * 64;
   constexpr int SL = (kSmRows * JW * WAVES * F::kBPC + T - 1) / T;   // scale loads per thread (upper bound)
   extern __shared__ uint16_t s_scale[];
-  __shared__ f32x4 red[WAVES - 1][2][64];
+  __shared__ f32x4 red[WAVES][2 * MT][64];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -110,9 +115,10 @@ __global__ __launch_bounds__(WAVES * 64) void smallm_kernel(SmallArgs a) {
     const uint32_t so = live ? ((uint32_t)(n0 + row) * (uint32_t)nblk + (uint32_t)(blk0 + blk)) * 2u : kOOB;
     sv[q] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(sr, so, 0, 0);
   }
-  // weights and activations, chunk by chunk, at most kSmDepth chunks of a wave in flight
+  // weights and activations, chunk by chunk, at most kSmDepth chunks of a wave in flight (fewer
+  // with several activation blocks, whose loads take MT times the registers)
   uint4 w[JW][2];
-  u32x4 xv[JW][U];
+  u32x4 xv[JW][MT][U];
   auto issue = [&](int j) {
     const int c = c_begin + wave + WAVES * j;
     const int kst = c * KC + g * EPL;          // first K element of this lane's load
@@ -124,13 +130,19 @@ __global__ __launch_bounds__(WAVES * 64) void smallm_kernel(SmallArgs a) {
       const uint32_t wo = live ? (uint32_t)n * rowbytes + (uint32_t)c * 64u + (uint32_t)g * 16u : kOOB;
       w[j][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wr, wo, 0, 0));
     }
-    const bool xok = ok && r16 < M;
-    const uint32_t xo = ((uint32_t)r16 * (uint32_t)K + (uint32_t)kst) * 2u;
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      xv[j][u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xok ? xo + 16u * u : kOOB, 0, 0));
+    for (int cb = 0; cb < MT; ++cb) {
+      const int m = 16 * cb + r16;
+      const bool xok = ok && m < M;
+      const uint32_t xo = ((uint32_t)m * (uint32_t)K + (uint32_t)kst) * 2u;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        xv[j][cb][u] =
+            __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xok ? xo + 16u * u : kOOB, 0, 0));
+    }
   };
-  constexpr int D = JW < kSmDepth<FMT> ? JW : kSmDepth<FMT>;
+  constexpr int kDepth = MT == 1 ? kSmDepth<FMT> : (MT == 2 ? 2 : 1);
+  constexpr int D = JW < kDepth ? JW : kDepth;
 #pragma unroll
   for (int j = 0; j < D; ++j) issue(j);
   __builtin_amdgcn_sched_barrier(0);   // keep these loads ahead of the first LDS write
@@ -142,7 +154,11 @@ __global__ __launch_bounds__(WAVES * 64) void smallm_kernel(SmallArgs a) {
   }
   __syncthreads();
 
-  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  f32x4 acc[2][MT];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int cb = 0; cb < MT; ++cb) acc[i][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int j = 0; j < JW; ++j) {
     const int c = c_begin + wave + WAVES * j;
@@ -167,9 +183,12 @@ __global__ __launch_bounds__(WAVES * 64) void smallm_kernel(SmallArgs a) {
         wu[3] = dequant_q4_unit(d.w, sf, s16, off);
       }
 #pragma unroll
-      for (int u = 0; u < U; ++u)
-        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wu[u]),
-                                                        __builtin_bit_cast(bf16x8_t, xv[j][u]), acc[i], 0, 0, 0);
+      for (int cb = 0; cb < MT; ++cb)
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          acc[i][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wu[u]),
+                                                              __builtin_bit_cast(bf16x8_t, xv[j][cb][u]), acc[i][cb],
+                                                              0, 0, 0);
     }
     if (j + D < JW) {
       __builtin_amdgcn_sched_barrier(0);
@@ -178,34 +197,36 @@ __global__ __launch_bounds__(WAVES * 64) void smallm_kernel(SmallArgs a) {
     }
   }
 
-  // waves 1.. hand their sums to wave 0, which adds them in wave order
-  if (wave > 0) {
-    red[wave - 1][0][lane] = acc[0];
-    red[wave - 1][1][lane] = acc[1];
-  }
-  __syncthreads();
-  if (wave > 0) return;
+  // every wave hands its sums over through LDS; piece b (row group b / MT, column block b % MT) is
+  // then added by wave b % WAVES in wave order 0 .. WAVES-1 and stored by it
 #pragma unroll
-  for (int v = 0; v < WAVES - 1; ++v) {
-    acc[0] += red[v][0][lane];
-    acc[1] += red[v][1][lane];
-  }
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int cb = 0; cb < MT; ++cb) red[wave][i * MT + cb][lane] = acc[i][cb];
+  __syncthreads();
 
-  // lane holds output column m = r16 (activation row) and weight rows nb..nb+3 of each group;
-  // with K split over workgroups the partial goes to ws[s] and a second kernel sums the splits
-  const int m = r16;
-  if (m >= M) return;
-  float* dst = (a.splits == 1) ? a.y + (size_t)m * N : a.ws + ((size_t)s * M + m) * N;
+  // lane holds output column m = 16 cb + r16 (activation row) and weight rows nb..nb+3 of its
+  // piece; with K split over workgroups the partial goes to ws[s] and a second kernel sums the
+  // splits
   const bool vec = (N & 3) == 0;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int b0 = 0; b0 < 2 * MT; b0 += WAVES) {
+    const int b = b0 + wave;
+    if (b >= 2 * MT) break;
+    f32x4 sum = red[0][b][lane];
+#pragma unroll
+    for (int v = 1; v < WAVES; ++v) sum += red[v][b][lane];
+    const int i = b / MT, cb = b % MT;
+    const int m = 16 * cb + r16;
+    if (m >= M) continue;
+    float* dst = (a.splits == 1) ? a.y + (size_t)m * N : a.ws + ((size_t)s * M + m) * N;
     const int nb = n0 + 16 * i + 4 * g;
     if (vec && nb + 3 < N) {
-      *reinterpret_cast<f32x4*>(dst + nb) = acc[i];
+      *reinterpret_cast<f32x4*>(dst + nb) = sum;
     } else {
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        if (nb + r < N) dst[nb + r] = acc[i][r];
+        if (nb + r < N) dst[nb + r] = sum[r];
     }
   }
 }

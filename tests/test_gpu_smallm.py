@@ -1,8 +1,9 @@
-"""GPU parity of the small-M dense path (``qgemm_dense`` with M <= 16) against the fp64 oracle.
+"""GPU parity of the small-M dense path against the fp64 oracle: ``qgemm_dense`` with M <= 16, and
+with 16 < M <= 128 when the 128x128 tiles would occupy few CUs (then in blocks of 16 columns).
 
-Small M is the decode / speculative-verification shape: every weight is read once and dequantised
-straight into MFMA operand registers, K is split over waves and workgroups, and the partial sums
-are added in a fixed order. Bar: ``|y - y_ref| <= 1e-3 * sum_k |x_k w_k| + 1e-6`` elementwise,
+Small M is the decode / speculative-verification shape (and a short prompt's): every weight is read
+once and dequantised straight into MFMA operand registers, K is split over waves and workgroups,
+and the partial sums are added in a fixed order. Bar: ``|y - y_ref| <= 1e-3 * sum_k |x_k w_k| + 1e-6`` elementwise,
 plus the fp32-summation bound against the oracle with bf16-rounded weights.
 """
 import numpy as np
@@ -43,7 +44,7 @@ SHAPES = [(1, 32), (17, 64), (33, 96), (100, 224), (257, 1056), (31, 2048 + 96),
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-@pytest.mark.parametrize("M", [1, 2, 3, 5, 8, 12, 15, 16, 17])
+@pytest.mark.parametrize("M", [1, 2, 3, 5, 8, 12, 15, 16, 17, 24, 32, 33, 48, 64, 100, 128])
 @pytest.mark.parametrize("N,K", SHAPES)
 def test_small_m_shapes(fmt, M, N, K):
     torch = torch_or_skip()
@@ -61,6 +62,19 @@ def test_small_m_full_size(fmt, N, K, M):
     case = synth.dense_case(f"small_full_{synth.FMT_NAMES[fmt]}_{M}x{N}x{K}", fmt, M, N, K, seed=9,
                             stream=(M, N, K))
     check(case, run(torch, case).cpu().numpy(), require_bar=True)
+
+
+@pytest.mark.parametrize("M,fmt,N,K", [(128, synth.FMT_Q8, 1024, 1024), (96, synth.FMT_Q4, 2048, 3072),
+                                       (40, synth.FMT_Q8, 4096, 2048), (128, synth.FMT_Q4, 512, 8192)])
+def test_wide_small_m_full(M, fmt, N, K):
+    """Short-prompt shapes on the blocks-of-16-columns path, every output against the oracle and
+    bitwise repeatable."""
+    torch = torch_or_skip()
+    case = synth.dense_case(f"wide_{synth.FMT_NAMES[fmt]}_{M}x{N}x{K}", fmt, M, N, K, seed=14, stream=(M, N, K))
+    y = run(torch, case).cpu().numpy()
+    check(case, y, require_bar=True)
+    y2 = run(torch, case).cpu().numpy()
+    assert np.array_equal(y.view(np.uint32), y2.view(np.uint32))
 
 
 def test_small_m_deterministic_across_split_counts():
