@@ -116,7 +116,6 @@ __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (
 #define QG_PINGPONG 1
 #endif
 
-
 // Groups the ping-pong DMA-role step splits its activation DMA into, each followed by a share of
 // its dequantisation (0: all loads first, then all dequantisation)
 #ifndef QG_VMEM_SPLIT
