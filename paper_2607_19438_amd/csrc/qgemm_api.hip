@@ -187,9 +187,34 @@ int dense_dispatch(qg::TileArgs a, const void* wq, const void* sc, hipStream_t s
   a.splits = 1;
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
   if (a.M >= 256 && a.N >= 256 && big >= 200) return launch_dense<FMT, 256, 256, 2, 4, 2>(a, wq, sc, s);
+  const int nk = (a.K + 63) / 64;
+  // up to 1024 rows with few 256x256 tiles: 128x256 eight-wave tiles, twice the tiles, so half the
+  // K split and half the fp32 partials; the split keeps tiles x splits <= 256 (one round). Up to
+  // 2048 rows only where these tiles need no split. Measured against the 256x256 split: dense Q4
+  // 512x8192x3072 48-49 vs 51-53 us, Q8 512x2048x2048 26.6 vs 34.4, Q4 768x1536x2048 27.0 vs 35.6,
+  // Q8 256x8192x2048 29.2 vs 36.8, Q8 2048x4096x2048 49.6 vs 60.8, Q4 1536x4096x4096 78 vs 97 us;
+  // Q8 2048x2048x8192 (two splits needed) 100 vs 92.7 us stays on the 256x256 split.
+  const long t2 = (long)((a.M + 127) / 128) * ((a.N + 255) / 256);
+  if (a.M >= 128 && a.N >= 256 && ((long)a.M * a.N) % 4 == 0 && (a.M <= 1024 || (a.M <= 2048 && t2 > 128))) {
+    int S = (int)std::max<long>(1, std::min<long>(8, 256 / t2));
+    while (S > 1 && nk / S < kMinStepsPerSplit) --S;
+    if (S == 1) return launch_dense<FMT, 128, 256, 2, 4, 2>(a, wq, sc, s);
+    const long mn = (long)a.M * a.N;
+    std::lock_guard<std::mutex> lock(g_split_mutex);
+    float* ws = nullptr;
+    int rc = split_workspace((size_t)S * mn, &ws);
+    if (rc != QGEMM_OK) return rc;
+    a.ws = ws;
+    a.splits = S;
+    rc = launch_dense<FMT, 128, 256, 2, 4, 2>(a, wq, sc, s);
+    if (rc != QGEMM_OK) return rc;
+    const long n4 = mn / 4;
+    hipLaunchKernelGGL(qg::splitk_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, ws, a.y, n4, S,
+                       mn);
+    return check_launch("qgemm_dense split-K reduction");
+  }
   // few 256x256 tiles but a long K: split K over several workgroups per tile (fp32 partials,
   // summed in split order by a second kernel) so that every CU gets a 256x256 tile
-  const int nk = (a.K + 63) / 64;
   if (a.M >= 256 && a.N >= 256 && ((long)a.M * a.N) % 4 == 0) {
     int S = (int)std::min<long>(8, (256 + big - 1) / big);
     while (S > 1 && nk / S < kMinStepsPerSplit) --S;

@@ -65,7 +65,9 @@ RAGGED = [
     (4096, 4096, 64),      # 256x256 tiles, exact
     (300, 1000, 1536),     # split-K over 2 workgroups per 256x256 tile, ragged M and N
     (1000, 700, 4096 + 32),  # split-K over 5, K tail inside the last split
-    (512, 512, 8192),      # split-K over 4 (the down-projection shape class)
+    (512, 512, 8192),      # split-K over 8 on 128x256 tiles (the down-projection shape class)
+    (1500, 4000, 160),     # 128x256 tiles above 1024 rows (no split), ragged M and N
+    (1100, 4352, 1056),    # the same with an odd K-step count and a K tail
 ]
 # every K-step count modulo the unrolled loop period (2 or 6 steps) and each K tail position,
 # on the 128x128 tile (M < 256) and the 256x256 tile
