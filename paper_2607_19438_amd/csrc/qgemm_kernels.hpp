@@ -85,21 +85,33 @@ __device__ __forceinline__ u32x4 dequant_q8_unit(uint32_t d0, uint32_t d1, float
                pack_bf16x2(f6 * s, f7 * s)};
 }
 
-// Q4: one dword of 8 nibbles (element 2b in the low nibble of byte b, 2b+1 in the
-// high nibble). The low nibbles are masked in place (u), the high nibbles masked in
-// place too (16 u), so each converts with one byte-select cvt; s16 = s / 16 is exact.
-__device__ __forceinline__ u32x4 dequant_q4_unit(uint32_t d, float s, float s16, float off) {
-  uint32_t lo = d & 0x0F0F0F0Fu;
-  uint32_t hi = d & 0xF0F0F0F0u;
-  asm volatile("" : "+v"(lo), "+v"(hi));   // keep the byte-select conversions below
-  const float l0 = (float)(lo & 0xFFu), l1 = (float)((lo >> 8) & 0xFFu);
-  const float l2 = (float)((lo >> 16) & 0xFFu), l3 = (float)(lo >> 24);
-  const float h0 = (float)(hi & 0xFFu), h1 = (float)((hi >> 8) & 0xFFu);
-  const float h2 = (float)((hi >> 16) & 0xFFu), h3 = (float)(hi >> 24);
-  return u32x4{pack_bf16x2(__builtin_fmaf(l0, s, off), __builtin_fmaf(h0, s16, off)),
-               pack_bf16x2(__builtin_fmaf(l1, s, off), __builtin_fmaf(h1, s16, off)),
-               pack_bf16x2(__builtin_fmaf(l2, s, off), __builtin_fmaf(h2, s16, off)),
-               pack_bf16x2(__builtin_fmaf(l3, s, off), __builtin_fmaf(h3, s16, off))};
+// Q4: one dword of 8 nibbles (element 2b in the low nibble of byte b, 2b+1 in the high nibble).
+// Each 16-bit half of (d & 0x000F000F), (d & 0x00F000F0) and the same masks of d >> 8 holds one
+// nibble n (times 1 or 16) and no exponent bits, i.e. the fp16 subnormal n * 2^-24 (or
+// 16 n * 2^-24). v_fma_mix_f32 widens an fp16 half exactly and computes
+//   n * 2^-24 * (s * 2^24) - 8 s  =  (n - 8) * s
+// with one rounding; (n - 8) * s (4 x 11 significant bits) is exact in fp32, as are s * 2^24,
+// s * 2^20 and -8 s for every fp16 scale s, so the product is the exact dequantised weight and only
+// the bf16 packing rounds (RNE). s24 = s * 2^24, s20 = s * 2^20, off = -8 s (all zero for a masked
+// chunk). 17 VALU instructions per 8 weights (fp16 denormals are kept: float_denorm_mode_16_64).
+__device__ __forceinline__ u32x4 dequant_q4_unit(uint32_t d, float s24, float s20, float off) {
+  typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+  const uint32_t d8 = d >> 8;
+  const f16x2 a = __builtin_bit_cast(f16x2, d & 0x000F000Fu);    // elements 0, 4
+  const f16x2 b = __builtin_bit_cast(f16x2, d & 0x00F000F0u);    // elements 1, 5 (times 16)
+  const f16x2 c = __builtin_bit_cast(f16x2, d8 & 0x000F000Fu);   // elements 2, 6
+  const f16x2 e = __builtin_bit_cast(f16x2, d8 & 0x00F000F0u);   // elements 3, 7 (times 16)
+  return u32x4{pack_bf16x2(__builtin_fmaf((float)a[0], s24, off), __builtin_fmaf((float)b[0], s20, off)),
+               pack_bf16x2(__builtin_fmaf((float)c[0], s24, off), __builtin_fmaf((float)e[0], s20, off)),
+               pack_bf16x2(__builtin_fmaf((float)a[1], s24, off), __builtin_fmaf((float)b[1], s20, off)),
+               pack_bf16x2(__builtin_fmaf((float)c[1], s24, off), __builtin_fmaf((float)e[1], s20, off))};
+}
+
+// Q4 per-chunk factors of dequant_q4_unit from the fp16 scale s (0 for a masked chunk)
+__device__ __forceinline__ void q4_factors(float s, float& s24, float& s20, float& off) {
+  s24 = s * 16777216.0f;
+  s20 = s * 1048576.0f;
+  off = -8.0f * s;
 }
 
 // s_waitcnt vmcnt(n) expcnt(7) lgkmcnt(0) (gfx9 encoding)
@@ -334,7 +346,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   constexpr int kPeriod = (XS == 3 || kWD == 3) ? 6 : (kWD == 4 ? 4 : 2);
   static_assert(kUnits % 4 == 0, "units must spread evenly over the four K16 sub-steps");
   constexpr int kMfmaPerKK = KT::kTM * KT::kTN;
-  constexpr int kValuPerUnit = (FMT == kQ8) ? 20 : 22;
+  constexpr int kValuPerUnit = (FMT == kQ8) ? 20 : 17;
 
   // Ping-pong (8-wave tiles): the two waves sharing a SIMD belong to different wave rows (wm).
   // Per K step, wm = 1 waves issue the activation DMA while wm = 0 waves run their MFMAs; after
@@ -475,6 +487,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   };
 
   // dequantise unit u (0 <= u < kUnits) of a weight register set into LDS stage `stage`
+  // Q8: scl = s; Q4: scl = s * 2^24, scl16 = s * 2^20, soffv = -8 s (dequant_q4_unit)
   float scl[WC], scl16[WC], soffv[WC];
   auto dequant_unit = [&](int kt, int u, const uint4 (&w)[WC], const uint32_t (&s)[WC], int stage) {
     const int i = u / kUnitsPerChunk;
@@ -482,10 +495,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     if (sub == 0) {
       const bool valid = wrow_ok[i] && (ks0 + kt) * kBK + wcol[i] * KT::kWChunkElems < K;
       scl[i] = valid ? fp16_to_f32((uint16_t)s[i]) : 0.0f;
-      if constexpr (FMT == kQ4) {
-        scl16[i] = scl[i] * 0.0625f;
-        soffv[i] = -8.0f * scl[i];
-      }
+      if constexpr (FMT == kQ4) q4_factors(scl[i], scl[i], scl16[i], soffv[i]);
     }
     const uint32_t d[4] = {w[i].x, w[i].y, w[i].z, w[i].w};
     u32x4 o;

@@ -175,12 +175,12 @@ __global__ __launch_bounds__(WAVES * 64) void smallm_kernel(SmallArgs a) {
         wu[0] = dequant_q8_unit(d.x, d.y, sf);
         wu[1] = dequant_q8_unit(d.z, d.w, sf);
       } else {
-        const float s16 = sf * 0.0625f;
-        const float off = -8.0f * sf;
-        wu[0] = dequant_q4_unit(d.x, sf, s16, off);
-        wu[1] = dequant_q4_unit(d.y, sf, s16, off);
-        wu[2] = dequant_q4_unit(d.z, sf, s16, off);
-        wu[3] = dequant_q4_unit(d.w, sf, s16, off);
+        float s24, s20, off;
+        q4_factors(sf, s24, s20, off);
+        wu[0] = dequant_q4_unit(d.x, s24, s20, off);
+        wu[1] = dequant_q4_unit(d.y, s24, s20, off);
+        wu[2] = dequant_q4_unit(d.z, s24, s20, off);
+        wu[3] = dequant_q4_unit(d.w, s24, s20, off);
       }
 #pragma unroll
       for (int cb = 0; cb < MT; ++cb)
