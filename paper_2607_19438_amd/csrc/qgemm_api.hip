@@ -365,7 +365,7 @@ int moe_args_check(const void* x, const void* idx_or_perm, const int32_t* offset
   if (E > kMaxE) return fail(QGEMM_EUNSUPPORTED, "E = %d exceeds the supported %d experts", E, kMaxE);
   if (topk < 1 || topk > E) return fail(QGEMM_EINVAL, "topk must lie in [1, E] (got %d)", topk);
   if ((long)T * topk > 0x7fffffffL) return fail(QGEMM_EUNSUPPORTED, "T*topk too large");
-  if ((long)T * topk * N > 0x7fffffffffffL || (long)T * K > 0x7fffffffL)
+  if ((long)T * topk * N > 0x7fffffffffffL || (long)T * K > 0x7fffffffL || ((long)T + 1) * K * 2 + 256 >= 0xFFFFFFF0L)
     return fail(QGEMM_EUNSUPPORTED, "problem too large");
   if (T == 0) return QGEMM_OK;
   if (!x || !idx_or_perm || !offsets || !wq || !scales || !y) return fail(QGEMM_EINVAL, "null pointer argument");

@@ -402,7 +402,10 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
     for (int j = 0; j < XL; ++j) {
       const int r = xgroup(j) * 8 + (lane >> 3);
       const int src = (r < rows_valid) ? s_xrow[r] : -1;
-      xoff[j] = (src >= 0) ? (uint32_t)src * (uint32_t)K * 2u + (uint32_t)dma_c[j] * 16u : kOOB;
+      // a missing row gets an offset that stays past the buffer for every K step's byte offset
+      // added to it (the host keeps (T + 1) * K * 2 + 256 below kOOB)
+      xoff[j] = (src >= 0) ? (uint32_t)src * (uint32_t)K * 2u + (uint32_t)dma_c[j] * 16u
+                           : kOOB - 2u * (uint32_t)K - 2u * (uint32_t)kRowBytes;
     }
   } else {
     xr = make_rsrc(a.x + (size_t)m0 * K, (uint32_t)rows_valid * (uint32_t)K * 2u);
@@ -450,21 +453,32 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   // Loads of steps past this tile's last one (kt_local >= nk) are issued with out-of-range
   // offsets: the buffer range check answers them with zeros, no memory is read, and the K loop
   // stays free of branches around its loads.
+  // A step wholly inside K (every step but a ragged last one and the steps past the end) needs
+  // one address add per load; chunks past K and steps past the last one read nothing.
   auto issue_x = [&](int kt_local, int stage, int j0 = 0, int j1 = 1 << 30) {
     const int kt = ks0 + kt_local;
     const uint32_t kbyte = (uint32_t)kt * (uint32_t)kRowBytes;
     const bool tail = (kt + 1) * kBK > K || kt_local >= nk;
+    auto issue = [&](bool checked) {
 #pragma unroll
-    for (int j = 0; j < XL; ++j) {
-      if (j < j0 || j >= j1) continue;
-      // an 8-row group wholly past the valid rows is not fetched at all: its LDS rows keep
-      // stale data, which only reaches accumulator rows that are never stored. (With three
-      // stages the waits count this step's activation loads, so every group is issued.)
-      if (!FULL && XS == 2 && xgroup(j) * 8 >= rows_valid) continue;
-      uint32_t off = (xoff[j] == kOOB) ? kOOB : xoff[j] + kbyte;
-      if (tail && (kt_local >= nk || kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
-      lds_char* dst = xstage_ptr(stage) + xgroup(j) * 1024;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
+      for (int j = 0; j < XL; ++j) {
+        if (j < j0 || j >= j1) continue;
+        // an 8-row group wholly past the valid rows is not fetched at all: its LDS rows keep
+        // stale data, which only reaches accumulator rows that are never stored. (With three
+        // stages the waits count this step's activation loads, so every group is issued.)
+        if (!FULL && XS == 2 && xgroup(j) * 8 >= rows_valid) continue;
+        uint32_t off = xoff[j] + kbyte;
+        if (checked && (kt_local >= nk || kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
+        lds_char* dst = xstage_ptr(stage) + xgroup(j) * 1024;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
+      }
+    };
+    // (MoE tiles branch on the uniform flag; for dense tiles the branch measured slower than
+    // keeping the checks inline)
+    if constexpr (MOE) {
+      if (tail) issue(true); else issue(false);
+    } else {
+      issue(tail);
     }
   };
 
