@@ -467,10 +467,18 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
         // stale data, which only reaches accumulator rows that are never stored. (With three
         // stages the waits count this step's activation loads, so every group is issued.)
         if (!FULL && XS == 2 && xgroup(j) * 8 >= rows_valid) continue;
-        uint32_t off = xoff[j] + kbyte;
-        if (checked && (kt_local >= nk || kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
         lds_char* dst = xstage_ptr(stage) + xgroup(j) * 1024;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
+        if (MOE && !checked) {
+          // the step's byte offset rides in the scalar offset: no vector address arithmetic
+          // (the row offset alone decides the range check, whether or not the hardware adds
+          // the scalar offset to it: missing rows stay past the buffer either way)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, xoff[j],
+                                                   (int)kbyte, 0, 0);
+        } else {
+          uint32_t off = xoff[j] + kbyte;
+          if (checked && (kt_local >= nk || kt * kBK + dma_c[j] * 8 >= K)) off = kOOB;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
+        }
       }
     };
     // (MoE tiles branch on the uniform flag; for dense tiles the branch measured slower than
