@@ -83,6 +83,10 @@ def test_moe_host_validation(qmod):
     assert "expert 2" in qmod.last_error()
     assert lib.qgemm_moe(16, 16, 16, ptrs, ptrs, 16, 0, 4, 2, 128, 64, 0, None) == 0       # T == 0
     assert lib.qgemm_moe(0, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 128, 64, 0, None) == -1       # null x
+    # activations within 2^31 elements but (T + 1) * K * 2 bytes at 4 GiB: the 32-bit activation
+    # offsets (and the out-of-range offset of a missing row) no longer fit
+    assert lib.qgemm_moe(16, 16, 16, ptrs, ptrs, 16, (1 << 20) - 1, 4, 2, 128, 2048, 0, None) == -3
+    assert "too large" in qmod.last_error()
     assert lib.qgemm_moe_grouped(16, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 128, 64, 9, None) == -1
     assert lib.qgemm_moe_gate_up_swiglu(16, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 0, 64, 0, None) == -1   # inter < 1
     assert lib.qgemm_moe_gate_up_swiglu(16, 16, 16, ptrs, ptrs, 16, 4, 4, 2, 64, 48, 0, None) == -1  # K % 32
