@@ -360,13 +360,11 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   // Weight chunks per thread: without ping-pong every thread takes kWChunks. With it the wm = 0
   // waves take CQ chunks (dequantised after their MFMA phase) and the wm = 1 waves CD chunks
   // (dequantised in their DMA phase).
-#ifndef QG_Q_ALL_Q8
-#define QG_Q_ALL_Q8 0
-#endif
   // Q4: the wm = 0 waves dequantise every chunk (their phase after the MFMAs had the slack; the
   // DMA role's phase is then the activation DMA and its fragment loads only): 488.7 vs 493.5 us
-  // (T=8192 gate/up), 158.1 vs 164.2 us (T=2048 gate/up), same-box A/B
-  constexpr int CQ = PP ? ((FMT == kQ4 || QG_Q_ALL_Q8) ? 2 * KT::kWChunks
+  // (T=8192 gate/up), 158.1 vs 164.2 us (T=2048 gate/up), same-box A/B; Q8 keeps its 3:1 split
+  // (dense 0.8% slower with every chunk on one role)
+  constexpr int CQ = PP ? ((FMT == kQ4) ? 2 * KT::kWChunks
                                                        : (KT::kWChunks >= 2 ? (3 * KT::kWChunks + 1) / 2 : KT::kWChunks))
                         : KT::kWChunks;
   constexpr int CD = PP ? 2 * KT::kWChunks - CQ : KT::kWChunks;
