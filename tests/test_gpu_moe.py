@@ -38,6 +38,8 @@ def run_moe(torch, x, r, ws, fmt):
     (1, 1, 1, 128, 32, 0.0), (37, 5, 2, 160, 96, 0.0), (300, 16, 4, 256, 128, 1.2),
     (513, 8, 8, 96, 64, 0.0), (1000, 130, 3, 128, 64, 1.0),     # E > 128: two launches
     (200, 6, 2, 384, 768, 0.5),
+    (600, 2, 2, 256, 160, 0.0),     # 256x256 ping-pong tiles, ragged last K step
+    (400, 4, 1, 256, 224, 0.0),     # 192x256 ping-pong tiles, ragged last K step
 ])
 def test_grouped_small_full(fmt, T, E, topk, N, K, skew):
     torch = torch_or_skip()
