@@ -198,7 +198,9 @@ struct TileKernel {
   static constexpr int kWTN = BN / WN;        // cols per wave
   static constexpr int kTM = kWTM / 32;       // 32x32 MFMA blocks per wave (M)
   static constexpr int kTN = kWTN / 32;       // (N)
-  static constexpr int kXLoads = BM / 8 / kWaves;               // 1 KiB LDS-DMA loads (8 rows) per wave per K step
+  static constexpr int kXGroups = BM / 8;                         // 8-row groups (1 KiB LDS-DMA loads) per K step
+  static constexpr int kXWaves = kXGroups < kWaves ? kXGroups : kWaves;   // waves that issue them
+  static constexpr int kXLoads = kXGroups / kXWaves;              // per DMA wave per K step
   static constexpr int kWChunkElems = (FMT == kQ8) ? 16 : 32;   // weights per 16-byte load
   static constexpr int kWChunksPerRow = kBK / kWChunkElems;     // 4 (Q8) or 2 (Q4)
   static constexpr int kWStepBytes = (FMT == kQ8) ? kBK : kBK / 2;   // packed bytes of one row per K step
@@ -209,7 +211,7 @@ struct TileKernel {
   static constexpr int kWBase = XS * kXTileBytes;                 // weight stages follow the activation stages
   static constexpr int kLdsBytes = XS * kXTileBytes + 2 * kWTileBytes;
   static_assert(XS == 2 || XS == 3, "two or three activation stages");
-  static_assert(kXLoads * kWaves * 8 == BM, "x tile must split into 8-row groups per wave");
+  static_assert(kXLoads * kXWaves * 8 == BM, "x tile must split into 8-row groups per wave");
   static_assert(kWChunks * kThreads == BN * kWChunksPerRow, "w tile must split evenly");
   static_assert(kTM >= 1 && kTN >= 1, "wave tile must hold a 32x32 block");
 };
@@ -475,6 +477,7 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
         // stale data, which only reaches accumulator rows that are never stored. (With three
         // stages the waits count this step's activation loads, so every group is issued.)
         if (!FULL && XS == 2 && xgroup(j) * 8 >= rows_valid) continue;
+        if (KT::kXWaves < KT::kWaves && xgroup(j) >= KT::kXGroups) continue;   // a wave without DMA
         lds_char* dst = xstage_ptr(stage) + xgroup(j) * 1024;
         if (MOE && !checked) {
           // the step's byte offset rides in the scalar offset: no vector address arithmetic
@@ -1127,8 +1130,20 @@ __global__ __launch_bounds__(WM * WN * 64, WM * WN == 4 ? (BM <= 64 ? 3 : 2) : 1
     s_xrow[r] = asg < 0 ? -1 : asg / a.topk;
   }
   __syncthreads();
+  const int nk = (a.K + kBK - 1) / kBK;
+  if constexpr (WM == 2 && WN == 4) {
+    // A group of at most 32 rows (a small expert, or the last rows of a large one) has MFMA work
+    // for one wave row only, while the whole tile's weights still need dequantising: such a tile
+    // runs as 32 rows by BN over all eight waves side by side, each dequantising an eighth of the
+    // weights, on the single-barrier loop (same products in the same order, so the same bits).
+    if (rows_valid <= 32) {
+      tile_dispatch<FMT, 32, BN, 1, 8, true, 2, SWI, CMB>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow,
+                                                         s_rowidx, lds, 0, nk, a.y);
+      return;
+    }
+  }
   tile_dispatch<FMT, BM, BN, WM, WN, true, XS, SWI, CMB>(a, ep.wq[e], ep.sc[e], 0, nt * BN, rows_valid, s_xrow,
-                                                         s_rowidx, lds, 0, (a.K + kBK - 1) / kBK, a.y);
+                                                         s_rowidx, lds, 0, nk, a.y);
 }
 
 }  // namespace qg

@@ -196,3 +196,45 @@ def test_tile_choice_boundary_bitwise(fmt):
     n = idx_a.size
     assert np.array_equal(ys[0].view(np.uint32), ys[1][:n].view(np.uint32))
     assert np.array_equal(hs[0], hs[1][:n])
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_small_groups_in_eight_wave_launches_bitwise(fmt):
+    """Small experts (1, 17, 20, 32 rows) and the short last groups of large ones beside a 33-row
+    expert, in launches of 256x256 tiles (1544 rows over 8 experts: mean 193; 900 = 3 x 256 + 132,
+    541 = 2 x 256 + 29) and of 192x256 tiles (the same routing over 9 experts: mean 171; 900 =
+    4 x 192 + 132, 541 = 2 x 192 + 157). Plain and fused SwiGLU results meet the oracle's bar and
+    are bitwise equal to the same routing over 49 experts (mean 31), which takes the four-wave
+    tiles."""
+    torch = torch_or_skip()
+    m = q()
+    K, inter = 512, 128
+    counts = [900, 1, 32, 33, 0, 17, 541, 20]
+    rng = synth.rng_for(29, fmt, *counts)
+    idx = np.repeat(np.arange(len(counts), dtype=np.int32), counts)
+    rng.shuffle(idx)
+    x = synth.make_x(rng, idx.size, K)
+    ws = [synth.make_qweight(rng, 2 * inter, K, fmt) for _ in counts]
+    ys, hs = [], []
+    for E in (8, 9, 49):
+        wse = ws + [ws[0]] * (E - len(ws))              # experts past the routed ones stay empty
+        wq, sc = dev_experts(torch, wse)
+        table = m.ExpertTable(wq, sc, fmt)
+        r = synth.routing_from_idx(idx, E, 1, np.ones(idx.size, np.float32))
+        off = dev_i32(torch, r.expert_offsets)
+        perm = m.moe_bucket(dev_i32(torch, r.token_expert_idx), off)
+        y = m.moe_grouped(dev_x(torch, x), perm, off, table, None, 1, fmt)
+        h = m.moe_gate_up_swiglu(dev_x(torch, x), perm, off, table, None, 1, fmt)
+        torch.cuda.synchronize()
+        y = y.cpu().numpy()
+        check(f"moe small groups E={E} {synth.FMT_NAMES[fmt]}", x, r, wse, fmt, y, K)
+        hb = h.cpu().view(torch.int16).numpy().view(np.uint16)
+        y1b, b1b = oracle.moe(x, r.token_expert_idx, r.expert_offsets, [w.wq for w in wse],
+                              [w.scales for w in wse], 1, fmt, bf16_weights=True)
+        h_ref, _ = oracle.swiglu(y1b, inter)
+        tol = oracle.swiglu_err_bound(y1b, b1b, inter, rel=oracle.fp32_sum_rel(K), abs_=1e-30)
+        assert float(np.max(np.abs(oracle.decode_bf16(hb) - h_ref) / (tol + 1e-30))) <= 1.0
+        ys.append(y.view(np.uint32))
+        hs.append(hb)
+    for i in (0, 1):
+        assert np.array_equal(ys[i], ys[2]) and np.array_equal(hs[i], hs[2])
