@@ -54,6 +54,8 @@ def bits(a):
     (64, 12, 10, 512, 64, 0.3),       # topk > 8: slots in two groups
     (100, 64, 4, 384, 768, 0.5),      # mean 6 rows per expert: four-wave 128x128 tiles
     (200, 6, 2, 2048, 768, 0.5),      # the down projection's N and K
+    (700, 4, 2, 256, 128, 3.0),       # 256x256 tiles (mean 350) beside a 27/28-row expert: 32-row tile
+    (900, 4, 1, 512, 160, 3.0),       # 256x256 tiles, experts of 1-5 rows, two column tiles, ragged K
 ])
 def test_fused_equals_grouped_plus_combine(fmt, T, E, topk, N, K, skew):
     torch = torch_or_skip()

@@ -199,19 +199,19 @@ def test_tile_choice_boundary_bitwise(fmt):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-@pytest.mark.parametrize("inter", [128, 384])
-def test_small_groups_in_eight_wave_launches_bitwise(fmt, inter):
+@pytest.mark.parametrize("inter,K", [(128, 512), (384, 512), (128, 160)])
+def test_small_groups_in_eight_wave_launches_bitwise(fmt, inter, K):
     """Small experts (1, 17, 20, 32 rows) and the short last groups of large ones beside a 33-row
     expert, in launches of 256x256 tiles (1544 rows over 8 experts: mean 193; 900 = 3 x 256 + 132,
     541 = 2 x 256 + 29) and of 192x256 tiles (the same routing over 9 experts: mean 171; 900 =
     4 x 192 + 132, 541 = 2 x 192 + 157). Plain and fused SwiGLU results meet the oracle's bar and
     are bitwise equal to the same routing over 49 experts (mean 31), which takes the four-wave
-    tiles. inter = 384 gives three 256-column tiles (plain and gate/up), an odd count."""
+    tiles. inter = 384 gives three 256-column tiles (plain and gate/up), an odd count; K = 160 ends
+    in half a K step."""
     torch = torch_or_skip()
     m = q()
-    K = 512
     counts = [900, 1, 32, 33, 0, 17, 541, 20]
-    rng = synth.rng_for(29, fmt, inter, *counts)
+    rng = synth.rng_for(29, fmt, inter, K, *counts)
     idx = np.repeat(np.arange(len(counts), dtype=np.int32), counts)
     rng.shuffle(idx)
     x = synth.make_x(rng, idx.size, K)
