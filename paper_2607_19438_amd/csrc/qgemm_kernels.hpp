@@ -7,7 +7,8 @@
 // Q8 / Q4 weights are read from HBM with 16-byte loads, dequantised in
 // registers (value * fp16 block scale, rounded to bf16) and staged in LDS so
 // every wave of the workgroup reuses them. Activations are staged in LDS too.
-// LDS is double-buffered: the four-wave tiles close a 64-wide K step with one
+// LDS is double-buffered: the single-barrier tiles (four waves, or eight waves
+// side by side on 32 rows for small MoE groups) close a 64-wide K step with one
 // barrier, the eight-wave ping-pong tiles with two (see tile_body).
 #pragma once
 
@@ -324,7 +325,7 @@ __device__ __forceinline__ void combine_arrivals(const TileArgs& a, __amdgpu_buf
 // One output tile: rows [m0, m0 + rows_valid) of x (dense) or the gathered rows
 // s_xrow[] (MoE), columns [n0, n0 + BN) of W.
 //
-// Pipeline per 64-wide K step kt of the four-wave tiles (two LDS stages, kWD weight register
+// Pipeline per 64-wide K step kt of the single-barrier tiles (two LDS stages, kWD weight register
 // sets; the eight-wave ping-pong loop is described where it is built):
 //   issue activation DMA for step kt+1 into stage (kt+1)&1     (buffer_load ... lds)
 //   issue packed-weight + scale loads for step kt+kWD          (registers)
