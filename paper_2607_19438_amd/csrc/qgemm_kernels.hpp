@@ -346,7 +346,11 @@ __device__ __forceinline__ void tile_body(const TileArgs& a, const uint8_t* __re
   static_assert(!CMB || (MOE && !SWI), "the fused combine is a MoE down-projection epilogue");
   constexpr int kUnitsPerChunk = (FMT == kQ8) ? 2 : 4;        // 16-byte LDS writes per 16-byte load
   constexpr int kUnits = KT::kWChunks * kUnitsPerChunk;        // per thread per K step
-  constexpr int kWD = (FMT == kQ4) ? 3 : 2;                    // weight prefetch distance (K steps)
+  // weight prefetch distance (K steps): two, and three for the four-wave Q4 tiles (eight-wave Q4
+  // tiles at two instead of three: step -1.1%, T=2048 gate/up -2.7%, down -3.5%, T=8192 down -2%,
+  // no VGPR spills instead of 9-11 in the 256-row tiles; the four-wave short-prompt tiles
+  // 0-1% slower at two; Q8 at three: 108 spills in the dense 256x256 tile)
+  constexpr int kWD = (FMT == kQ4 && KT::kWaves == 4) ? 3 : 2;
   // the K loop is unrolled over a period in which activation stage, weight register set and
   // weight LDS stage (two) all repeat
   constexpr int kPeriod = (XS == 3 || kWD == 3) ? 6 : (kWD == 4 ? 4 : 2);
